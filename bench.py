@@ -1,0 +1,236 @@
+"""Throughput of the MLIP energy/force/virial path on one MI355X.
+
+A step is one velocity-Verlet NVE step of the whole path: half kick and drift,
+a neighbour-list rebuild every 10 steps (or earlier when an atom has moved
+more than skin/2), the fused energy/force/virial evaluation of every atom,
+and the second half kick.  Inputs are resident in HBM before timing starts.
+
+Default workload: 6-component equiatomic random FCC alloy, 128^3 cells =
+8,388,608 atoms, a = 3.6 A, sigma = 0.1 A, cutoff 6.0 A, skin 0.5 A, k = 32,
+l_max = 3, encoder 3 x 128, head 4 x 64, random N(0, 1/fan_in) weights.
+
+Prints one JSON line (rank 0, one GPU).
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_FP64_TFLOPS = 78.6   # MI355X dense FP64 (vector and matrix)
+PEAK_HBM_GBS = 8000.0
+
+
+def flops_per_pair(hp) -> float:
+    """Algorithmic FLOP per active pair: encoder forward and tangent
+    (2 x 2 x MAC) plus the moment and the two W contractions (6 d k)."""
+    W = hp.enc_width
+    mac_enc = W + (hp.enc_hidden - 1) * W * W + W * hp.k
+    d = (hp.lmax + 1) ** 2
+    return 4.0 * mac_enc + 6.0 * d * hp.k
+
+
+def flops_per_atom(hp) -> float:
+    """Algorithmic FLOP per atom for the energy head forward and backward."""
+    R = hp.reg_width
+    mac_head = (hp.lmax + 1) * hp.k * R + (hp.reg_hidden - 1) * R * R + R
+    return 4.0 * mac_head
+
+
+def log(msg: str) -> None:
+    print(msg, file=sys.stderr, flush=True)
+
+
+def _oracle_worker(args):
+    import threadpoolctl
+    with threadpoolctl.threadpool_limits(1):
+        from oracle.model import Model, evaluate
+        hp, weights, pos, types, box, off, idx, centres = args
+        m = Model(hp, weights)
+        t0 = time.perf_counter()
+        evaluate(m, pos, types, box, off, idx, centres=centres)
+        return time.perf_counter() - t0
+
+
+def cpu_baseline(w, target_atoms: int) -> dict:
+    """Oracle timed on this host's cores on a bounded sample of the workload:
+    the centre atoms inside a cube of the supercell, with neighbours taken
+    from the surrounding atoms (evaluation only, no neighbour search)."""
+    import multiprocessing as mp
+    from oracle.neighbors import neighbors_of
+
+    rl = w.hp.cutoff + w.hp.skin
+    box = w.box
+    c0 = box / 2.0
+    d = w.pos - c0
+    d -= box * np.round(d / box)
+    rho = len(w.pos) / float(np.prod(box))
+    half = 0.5 * (target_atoms / rho) ** (1.0 / 3.0)
+    inner = np.all(np.abs(d) < half, axis=1)
+    outer = np.all(np.abs(d) < half + rl + 0.5, axis=1)
+    loc = np.nonzero(outer)[0]
+    lpos = d[loc] + 500.0
+    ltypes = w.types[loc]
+    lbox = np.array([1000.0, 1000.0, 1000.0])
+    centres = np.nonzero(inner[loc])[0]
+    rows = neighbors_of(lpos, lbox, rl, range(len(lpos)))
+    off = np.zeros(len(lpos) + 1, dtype=np.int64)
+    np.cumsum([len(r) for r in rows], out=off[1:])
+    idx = np.concatenate(rows).astype(np.int32)
+    cores = min(16, len(os.sched_getaffinity(0)))
+    chunks = np.array_split(centres, cores)
+    jobs = [(w.hp, w.weights, lpos, ltypes, lbox, off, idx, c) for c in chunks if len(c)]
+    ctx = mp.get_context("fork")
+    t0 = time.perf_counter()
+    with ctx.Pool(len(jobs)) as pool:
+        pool.map(_oracle_worker, jobs)
+    wall = time.perf_counter() - t0
+    return {"value": len(centres) / wall, "unit": "atom-steps/s", "cores": len(jobs), "kind": "oracle",
+            "sample": f"{len(centres)} centre atoms of the same workload (a cube at the box centre), "
+                      f"one E+F+virial evaluation each, float64 NumPy, {len(jobs)} processes x 1 BLAS "
+                      f"thread, {wall:.1f} s wall; neighbour search not timed"}
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--workload", default="fcc-hea6-128")
+    ap.add_argument("--cells", type=int, default=None, help="supercell edge override (cells)")
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--rebuild-every", type=int, default=10)
+    ap.add_argument("--cpu-sample", type=int, default=3000, help="oracle sample size (atoms); 0 disables")
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              "(spatial decomposition across GPUs is described in DESIGN.md, not built)", file=sys.stderr)
+        return 2
+
+    import torch
+    import synth
+    from paper_2608_16329_amd import Potential
+
+    t_gen = time.perf_counter()
+    w = synth.make_workload(args.workload, seed=args.seed, n=args.cells)
+    N = len(w.pos)
+    log(f"[bench] workload {w.description}: N={N} generated in {time.perf_counter() - t_gen:.1f}s")
+    dev = torch.device("cuda:0")
+    torch.cuda.init()
+    free0, total_mem = torch.cuda.mem_get_info(dev)
+    pos = torch.from_numpy(w.pos).to(dev)
+    vel = torch.from_numpy(w.vel).to(dev)
+    types = torch.from_numpy(w.types).to(dev)
+    F = torch.zeros((N, 3), dtype=torch.float64, device=dev)
+    E = torch.zeros(N, dtype=torch.float64, device=dev)
+    V = torch.zeros((N, 9), dtype=torch.float64, device=dev)
+    ref = pos.clone()
+    stream = torch.cuda.current_stream()
+    pot = Potential(w.hp, w.weights, stream=stream)
+    pot.set_masses(w.masses)
+    t0 = time.perf_counter()
+    pot.build_neighbors(pos, types, w.box)
+    torch.cuda.synchronize()
+    t_build = time.perf_counter() - t0
+    pot.compute(pos, F, E, V)
+    torch.cuda.synchronize()
+    free1, _ = torch.cuda.mem_get_info(dev)
+    st = pot.stats()
+    log(f"[bench] build {t_build * 1e3:.1f} ms; stats {st}")
+
+    dt = w.dt
+    skin2 = (0.5 * w.hp.skin) ** 2
+    step_no = 0
+    rebuilds = 0
+    compute_ms = []
+
+    def md_step(timed: bool):
+        nonlocal step_no, rebuilds
+        step_no += 1
+        d2 = pot.md_first_half(pos, vel, F, dt, ref)
+        if step_no % args.rebuild_every == 0 or d2 > skin2:
+            pot.build_neighbors(pos, types, w.box)
+            ref.copy_(pos)
+            rebuilds += 1
+        if timed:
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            pot.compute(pos, F, E, V)
+            e1.record(stream)
+            compute_ms.append((e0, e1))
+        else:
+            pot.compute(pos, F, E, V)
+        pot.md_second_half(vel, F, dt)
+
+    for _ in range(args.warmup):
+        md_step(False)
+    torch.cuda.synchronize()
+    rebuilds = 0
+    active_pairs = []
+    t0 = time.perf_counter()
+    for k in range(args.steps):
+        md_step(True)
+        torch.cuda.synchronize()
+        active_pairs.append(pot.stats()["n_active_pairs"])
+        log(f"[bench] step {k + 1}/{args.steps} done, {time.perf_counter() - t0:.2f}s")
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    kern = [a.elapsed_time(b) for a, b in compute_ms]
+    ms_compute = float(np.mean(kern))
+    flop = float(np.mean(active_pairs)) * flops_per_pair(w.hp) + N * flops_per_atom(w.hp)
+    achieved = flop / (ms_compute * 1e-3) / 1e12
+    value = N * args.steps / wall
+    st = pot.stats()
+    lib_bytes = pot.memory_bytes()
+    caller_bytes = N * (24 + 24 + 4 + 24 + 8 + 72 + 24)  # pos, vel, types, F, E, virial, ref
+    used = free0 - free1
+    bpa = used / N
+
+    result = {
+        "metric": "atom-steps/s (E+F+virial) at 1 GPU",
+        "value": value,
+        "unit": "atom-steps/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": wall / args.steps * 1e3,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f64",
+        "data": "synthetic",
+        "config": {"workload": w.description, "n_atoms": N, "n_species": w.hp.n_species, "k": w.hp.k,
+                   "lmax": w.hp.lmax, "cutoff": w.hp.cutoff, "skin": w.hp.skin, "dt_fs": dt,
+                   "rebuild_every": args.rebuild_every, "rebuilds_in_timed_steps": rebuilds,
+                   "active_pairs_per_atom": float(np.mean(active_pairs)) / N,
+                   "listed_pairs_per_atom": st["n_listed_pairs"] / N, "tile_atoms": st["tile_atoms"],
+                   "blocks": st["n_blocks"], "seed": args.seed},
+        "roofline": {"bound": "mfma", "achieved": achieved, "peak": PEAK_FP64_TFLOPS, "unit": "TFLOP/s",
+                     "frac": achieved / PEAK_FP64_TFLOPS, "traffic": None,
+                     "kernel": "fused energy/force/virial (k_fused)", "kernel_ms": ms_compute,
+                     "algorithmic_flop_per_launch": flop},
+        "hbm_bytes_per_atom": bpa,
+        "library_bytes_per_atom": lib_bytes / N,
+        "caller_bytes_per_atom": caller_bytes / N,
+        "max_atoms_estimate": int(0.95 * total_mem / bpa),
+        "build_ms": t_build * 1e3,
+    }
+    if args.cpu_sample > 0:
+        log("[bench] timing the oracle on a bounded sample")
+        result["cpu_baseline"] = cpu_baseline(w, args.cpu_sample)
+    pot.close()
+    print(json.dumps(result), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

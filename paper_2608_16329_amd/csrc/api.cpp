@@ -1,0 +1,512 @@
+// C ABI of the MLIP library (declared in include/mlip.h): argument checks,
+// weight repacking into MFMA fragment order, device buffers, and the launch
+// sequence of the neighbour builder and the fused kernel.
+#include <algorithm>
+#include <cmath>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "mlip_internal.h"
+
+using namespace mlip;
+
+namespace mlip {
+size_t fused_smem_bytes(int k);
+}
+
+namespace {
+
+constexpr double kAccPerForceMass = 9.648533212e-3;  // (eV/A)/amu -> A/fs^2
+
+mlip_status fail(mlip_ctx* ctx, mlip_status st, const std::string& msg) {
+  if (ctx) ctx->err = msg;
+  return st;
+}
+
+mlip_status fail_hip(mlip_ctx* ctx, hipError_t e, const char* what) {
+  (void)hipGetLastError();
+  return fail(ctx, MLIP_E_HIP, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+#define MLIP_HIP(ctx, expr)                                  \
+  do {                                                       \
+    const hipError_t e_ = (expr);                            \
+    if (e_ != hipSuccess) return fail_hip((ctx), e_, #expr); \
+  } while (0)
+
+#define MLIP_TRY(expr)                    \
+  do {                                    \
+    const mlip_status s_ = (expr);        \
+    if (s_ != MLIP_OK) return s_;         \
+  } while (0)
+
+template <typename T>
+mlip_status ensure(mlip_ctx* ctx, T** p, size_t* cap, size_t need, const char* what) {
+  if (*p && need <= *cap) return MLIP_OK;
+  if (*p) {
+    (void)hipFree(*p);
+    ctx->bytes -= *cap * sizeof(T);
+    *p = nullptr;
+    *cap = 0;
+  }
+  if (need == 0) return MLIP_OK;
+  const hipError_t e = hipMalloc(reinterpret_cast<void**>(p), need * sizeof(T));
+  if (e != hipSuccess) {
+    *p = nullptr;
+    (void)hipGetLastError();
+    return fail(ctx, MLIP_E_OOM, std::string("device allocation failed: ") + what);
+  }
+  *cap = need;
+  ctx->bytes += need * sizeof(T);
+  return MLIP_OK;
+}
+
+template <typename T>
+void release(mlip_ctx* ctx, T** p, size_t cap) {
+  if (*p) {
+    (void)hipFree(*p);
+    ctx->bytes -= cap * sizeof(T);
+    *p = nullptr;
+  }
+}
+
+bool structurally_valid(const mlip_hparams* hp) {
+  return hp && hp->n_species >= 1 && hp->k >= 1 && hp->lmax >= 0 && hp->enc_width >= 1 &&
+         hp->enc_hidden >= 1 && hp->reg_width >= 1 && hp->reg_hidden >= 1 && hp->enc_cond >= 0 &&
+         hp->enc_cond <= 2 && hp->reg_cond >= 0 && hp->reg_cond <= 1 && (hp->angular == 0 || hp->angular == 1);
+}
+
+bool gpu_supported(const mlip_hparams* hp, std::string* why) {
+  if (hp->precision != 64) return *why = "precision must be 64", false;
+  if (hp->angular != 0) return *why = "only the irreducible angular basis runs on the GPU path", false;
+  if (hp->lmax < 0 || hp->lmax > 3) return *why = "lmax must be in 0..3 on the GPU path", false;
+  if (hp->k != 32) return *why = "k must be 32 on the GPU path", false;
+  if (hp->enc_width != kEncWidth) return *why = "enc_width must be 128 on the GPU path", false;
+  if (hp->reg_width != kHeadWidth) return *why = "reg_width must be 64 on the GPU path", false;
+  if (hp->enc_hidden < 1 || hp->enc_hidden > kMaxHidden) return *why = "enc_hidden must be in 1..8", false;
+  if (hp->reg_hidden < 1 || hp->reg_hidden > kMaxHidden) return *why = "reg_hidden must be in 1..8", false;
+  if (hp->n_species < 1 || hp->n_species > kMaxSpecies) return *why = "n_species must be in 1..16", false;
+  if (!(hp->cutoff > 0.0) || !std::isfinite(hp->cutoff)) return *why = "cutoff must be positive", false;
+  if (!(hp->skin >= 0.0) || !std::isfinite(hp->skin)) return *why = "skin must be non-negative", false;
+  return true;
+}
+
+size_t enc_tables(const mlip_hparams* hp) {
+  const size_t C = size_t(hp->n_species);
+  return hp->enc_cond == 2 ? C * C : (hp->enc_cond == 1 ? C : 1);
+}
+
+size_t head_tables(const mlip_hparams* hp) { return hp->reg_cond == 1 ? size_t(hp->n_species) : 1; }
+
+size_t enc_blob_doubles(const mlip_hparams* hp) {
+  const size_t W = size_t(hp->enc_width), k = size_t(hp->k);
+  return 2 * W + size_t(hp->enc_hidden - 1) * (W * W + W) + k * W + k;
+}
+
+size_t head_blob_doubles(const mlip_hparams* hp) {
+  const size_t R = size_t(hp->reg_width), nin = size_t(hp->lmax + 1) * size_t(hp->k);
+  return R * nin + R + size_t(hp->reg_hidden - 1) * (R * R + R) + R + 1;
+}
+
+// Fragment order of a [out][128] matrix for MFMA 16x16x4: block (T, i, t)
+// holds, at lane 16 g + c, element [16 t + c][16 T + 4 i + g].
+void pack_fragments(const double* M, int nout, std::vector<double>* out) {
+  const int tiles = nout / 16;
+  for (int T = 0; T < 8; ++T)
+    for (int i = 0; i < 4; ++i)
+      for (int t = 0; t < tiles; ++t)
+        for (int lane = 0; lane < 64; ++lane) {
+          const int g = lane >> 4, c = lane & 15;
+          out->push_back(M[size_t(16 * t + c) * kEncWidth + 16 * T + 4 * i + g]);
+        }
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t mlip_weight_count(const mlip_hparams* hp) {
+  if (!structurally_valid(hp)) return 0;
+  return enc_tables(hp) * enc_blob_doubles(hp) + head_tables(hp) * head_blob_doubles(hp);
+}
+
+mlip_status mlip_create(const mlip_hparams* hp, const double* weights_host, size_t n_weights, void* hip_stream,
+                        mlip_ctx** out) {
+  if (!out) return MLIP_E_ARG;
+  *out = nullptr;
+  if (!hp || !weights_host) return MLIP_E_ARG;
+  if (!structurally_valid(hp)) return MLIP_E_ARG;
+  std::string why;
+  if (!gpu_supported(hp, &why)) return MLIP_E_ARG;
+  if (n_weights != mlip_weight_count(hp)) return MLIP_E_ARG;
+
+  mlip_ctx* ctx = new mlip_ctx();
+  ctx->hp = *hp;
+  ctx->stream = reinterpret_cast<hipStream_t>(hip_stream);
+  if (hipGetDevice(&ctx->device) != hipSuccess ||
+      hipDeviceGetAttribute(&ctx->n_cu, hipDeviceAttributeMultiprocessorCount, ctx->device) != hipSuccess) {
+    (void)hipGetLastError();
+    delete ctx;
+    return MLIP_E_HIP;
+  }
+  const int k = hp->k;
+  const int nin = (hp->lmax + 1) * k;
+  ctx->n_enc = int(enc_tables(hp));
+  ctx->n_head = int(head_tables(hp));
+  ctx->enc_stride = enc_table_doubles(k, hp->enc_hidden);
+  ctx->head_stride = head_table_doubles(nin, hp->reg_hidden);
+
+  // encoder tables -> [w0 b0 | (fragments(W_t) b_t)... | fragments(W_out) b_out]
+  std::vector<double> enc;
+  enc.reserve(ctx->enc_stride * ctx->n_enc);
+  const double* src = weights_host;
+  const size_t W = kEncWidth;
+  for (int t = 0; t < ctx->n_enc; ++t) {
+    const double* p = src + size_t(t) * enc_blob_doubles(hp);
+    enc.insert(enc.end(), p, p + 2 * W);
+    p += 2 * W;
+    for (int h = 1; h < hp->enc_hidden; ++h) {
+      pack_fragments(p, kEncWidth, &enc);
+      enc.insert(enc.end(), p + W * W, p + W * W + W);
+      p += W * W + W;
+    }
+    pack_fragments(p, k, &enc);
+    enc.insert(enc.end(), p + size_t(k) * W, p + size_t(k) * W + k);
+  }
+  // head tables -> [A0^T | A0 | c0 | (A_t^T A_t c_t)... | a_out c_out]
+  std::vector<double> head;
+  head.reserve(ctx->head_stride * ctx->n_head);
+  const double* hsrc = src + size_t(ctx->n_enc) * enc_blob_doubles(hp);
+  const size_t R = kHeadWidth;
+  for (int t = 0; t < ctx->n_head; ++t) {
+    const double* p = hsrc + size_t(t) * head_blob_doubles(hp);
+    for (int in = 0; in < nin; ++in)
+      for (size_t o = 0; o < R; ++o) head.push_back(p[o * nin + in]);
+    head.insert(head.end(), p, p + R * nin);
+    head.insert(head.end(), p + R * nin, p + R * nin + R);
+    p += R * nin + R;
+    for (int h = 1; h < hp->reg_hidden; ++h) {
+      for (size_t in = 0; in < R; ++in)
+        for (size_t o = 0; o < R; ++o) head.push_back(p[o * R + in]);
+      head.insert(head.end(), p, p + R * R + R);
+      p += R * R + R;
+    }
+    head.insert(head.end(), p, p + R + 1);
+  }
+  double qc[kAngRows * kMonomials];
+  std::string err;
+  if (!build_angular_table(hp->lmax, qc, &err) || enc.size() != ctx->enc_stride * ctx->n_enc ||
+      head.size() != ctx->head_stride * ctx->n_head) {
+    delete ctx;
+    return MLIP_E_ARG;
+  }
+  size_t cap = 0, cap2 = 0, cap3 = 0, cap4 = 0, cap5 = 0, cap6 = 0, cap7 = 0, cap8 = 0;
+  mlip_status st = MLIP_OK;
+  if ((st = ensure(ctx, &ctx->d_enc, &cap, enc.size(), "encoder")) != MLIP_OK ||
+      (st = ensure(ctx, &ctx->d_head, &cap2, head.size(), "head")) != MLIP_OK ||
+      (st = ensure(ctx, &ctx->d_qc, &cap3, size_t(kAngRows * kMonomials), "tables")) != MLIP_OK ||
+      (st = ensure(ctx, &ctx->d_totals, &cap4, size_t(16), "totals")) != MLIP_OK ||
+      (st = ensure(ctx, &ctx->d_counters, &cap5, size_t(4), "counters")) != MLIP_OK ||
+      (st = ensure(ctx, &ctx->d_flags, &cap6, size_t(4), "flags")) != MLIP_OK ||
+      (st = ensure(ctx, &ctx->d_reduce, &cap7, size_t(4), "reduce")) != MLIP_OK ||
+      (st = ensure(ctx, &ctx->d_inv_mass, &cap8, size_t(kMaxSpecies), "masses")) != MLIP_OK) {
+    mlip_destroy(ctx);
+    return st;
+  }
+  if (hipMemcpy(ctx->d_enc, enc.data(), enc.size() * sizeof(double), hipMemcpyHostToDevice) != hipSuccess ||
+      hipMemcpy(ctx->d_head, head.data(), head.size() * sizeof(double), hipMemcpyHostToDevice) != hipSuccess ||
+      hipMemcpy(ctx->d_qc, qc, sizeof(qc), hipMemcpyHostToDevice) != hipSuccess) {
+    (void)hipGetLastError();
+    mlip_destroy(ctx);
+    return MLIP_E_HIP;
+  }
+  *out = ctx;
+  return MLIP_OK;
+}
+
+mlip_status mlip_build_neighbors(mlip_ctx* ctx, int64_t n_atoms, const double* pos_dev, const int32_t* types_dev,
+                                 const double box_host[3]) {
+  if (!ctx) return MLIP_E_ARG;
+  ctx->err.clear();
+  if (!pos_dev || !types_dev || !box_host) return fail(ctx, MLIP_E_ARG, "NULL argument");
+  if (n_atoms < 1 || n_atoms >= (int64_t(1) << 31)) return fail(ctx, MLIP_E_ARG, "n_atoms outside [1, 2^31)");
+  const double rl = ctx->hp.cutoff + ctx->hp.skin;
+  for (int d = 0; d < 3; ++d)
+    if (!(box_host[d] > 0.0) || !std::isfinite(box_host[d])) return fail(ctx, MLIP_E_BOX, "box edges must be positive");
+  const double lmin = std::min(box_host[0], std::min(box_host[1], box_host[2]));
+  if (!(rl <= 0.5 * lmin)) return fail(ctx, MLIP_E_BOX, "cutoff + skin exceeds half the smallest box edge");
+  ctx->built = false;
+  const int64_t n = n_atoms;
+  const int C = ctx->hp.n_species;
+  hipStream_t s = ctx->stream;
+
+  NbrGrid g{};
+  int64_t ncell = 1;
+  for (int d = 0; d < 3; ++d) {
+    g.box[d] = box_host[d];
+    g.half[d] = 0.5 * box_host[d];
+    g.nc[d] = int(std::max(1.0, std::floor(box_host[d] / (rl * (1.0 + 1e-9)))));
+  }
+  // keep the key space proportional to the atom count
+  while (int64_t(g.nc[0]) * g.nc[1] * g.nc[2] * C > 4 * n + 4096) {
+    int dmax = 0;
+    for (int d = 1; d < 3; ++d)
+      if (g.nc[d] > g.nc[dmax]) dmax = d;
+    g.nc[dmax] = std::max(1, g.nc[dmax] / 2);
+  }
+  for (int d = 0; d < 3; ++d) g.cell_scale[d] = g.nc[d] / box_host[d];
+  ncell = int64_t(g.nc[0]) * g.nc[1] * g.nc[2];
+  g.ncell = int(ncell);
+  g.C = C;
+  g.rl2 = rl * rl;
+  const int64_t nkeys = ncell * C;
+
+  size_t cap = size_t(ctx->cap_atoms);
+  size_t cap_i32 = cap, cap_perm = cap, cap_key = cap, cap_rc = cap, cap_sp = cap * 3, cap_off = cap ? cap + 1 : 0;
+  if (size_t(n) > cap) {
+    MLIP_TRY(ensure(ctx, &ctx->d_types, &cap_i32, size_t(n), "types"));
+    MLIP_TRY(ensure(ctx, &ctx->d_perm, &cap_perm, size_t(n), "perm"));
+    MLIP_TRY(ensure(ctx, &ctx->d_key, &cap_key, size_t(n), "keys"));
+    MLIP_TRY(ensure(ctx, &ctx->d_rowcnt, &cap_rc, size_t(n), "row counts"));
+    MLIP_TRY(ensure(ctx, &ctx->d_spos, &cap_sp, size_t(3 * n), "sorted positions"));
+    MLIP_TRY(ensure(ctx, &ctx->d_offsets, &cap_off, size_t(n + 1), "offsets"));
+    ctx->cap_atoms = n;
+  }
+  size_t cap_keys = ctx->cap_keys, cap_keys2 = ctx->cap_keys;
+  MLIP_TRY(ensure(ctx, &ctx->d_cell_count, &cap_keys, size_t(nkeys + 1), "cell counts"));
+  MLIP_TRY(ensure(ctx, &ctx->d_cell_start, &cap_keys2, size_t(nkeys + 1), "cell starts"));
+  ctx->cap_keys = std::min(cap_keys, cap_keys2);
+  const size_t scan_need = std::max(scan_tmp_elems(n), scan_tmp_elems(nkeys));
+  MLIP_TRY(ensure(ctx, &ctx->d_scan_tmp, &ctx->cap_scan, scan_need, "scan scratch"));
+
+  MLIP_HIP(ctx, hipMemcpyAsync(ctx->d_types, types_dev, size_t(n) * sizeof(int32_t), hipMemcpyDeviceToDevice, s));
+  MLIP_HIP(ctx, launch_fill_i32(ctx->d_cell_count, nkeys + 1, 0, s));
+  MLIP_HIP(ctx, launch_fill_i32(ctx->d_flags, 4, 0, s));
+  MLIP_HIP(ctx, launch_bin(pos_dev, ctx->d_types, n, g, ctx->d_key, ctx->d_cell_count, ctx->d_flags, s));
+  MLIP_HIP(ctx, launch_exclusive_scan_i32_to_i32(ctx->d_cell_count, nkeys, ctx->d_cell_start, ctx->d_scan_tmp, s));
+  MLIP_HIP(ctx, launch_fill_i32(ctx->d_cell_count, nkeys + 1, 0, s));
+  MLIP_HIP(ctx, launch_scatter(ctx->d_key, n, ctx->d_cell_start, ctx->d_cell_count, ctx->d_perm, s));
+  MLIP_HIP(ctx, launch_sort_segments(ctx->d_cell_start, nkeys, ctx->d_perm, s));
+  MLIP_HIP(ctx, launch_gather_sorted(pos_dev, ctx->d_perm, n, g, ctx->d_spos, s));
+  MLIP_HIP(ctx, launch_rows(ctx->d_spos, ctx->d_perm, n, g, ctx->d_cell_start, ctx->d_rowcnt, nullptr, nullptr,
+                            ctx->d_flags, false, s));
+  MLIP_HIP(ctx, launch_exclusive_scan_i32_to_i64(ctx->d_rowcnt, n, ctx->d_offsets, ctx->d_scan_tmp, s));
+
+  int64_t total = 0;
+  int32_t flags[4] = {0, 0, 0, 0};
+  int32_t sp[kMaxSpecies + 1];
+  MLIP_HIP(ctx, hipMemcpyAsync(&total, ctx->d_offsets + n, sizeof(int64_t), hipMemcpyDeviceToHost, s));
+  MLIP_HIP(ctx, hipMemcpyAsync(flags, ctx->d_flags, sizeof(flags), hipMemcpyDeviceToHost, s));
+  for (int sp_i = 0; sp_i <= C; ++sp_i)
+    MLIP_HIP(ctx, hipMemcpyAsync(&sp[sp_i], ctx->d_cell_start + int64_t(sp_i) * ncell, sizeof(int32_t),
+                                 hipMemcpyDeviceToHost, s));
+  MLIP_HIP(ctx, hipStreamSynchronize(s));
+  if (flags[0]) return fail(ctx, MLIP_E_TYPE, "species outside [0, n_species) or non-finite position");
+  if (flags[1] > kEntCap) return fail(ctx, MLIP_E_NBR_CAP, "a neighbour row is longer than 2048 entries");
+
+  size_t need = size_t(std::max<int64_t>(total, 1));
+  if (need > ctx->cap_idx) need = need + need / 8;  // slack for later builds
+  MLIP_TRY(ensure(ctx, &ctx->d_idx, &ctx->cap_idx, need, "neighbour list"));
+  MLIP_HIP(ctx, launch_rows(ctx->d_spos, ctx->d_perm, n, g, ctx->d_cell_start, ctx->d_rowcnt, ctx->d_offsets,
+                            ctx->d_idx, ctx->d_flags, true, s));
+
+  ctx->grid = g;
+  ctx->n = n;
+  for (int d = 0; d < 3; ++d) ctx->box[d] = box_host[d];
+  for (int i = 0; i <= C; ++i) ctx->species_start[i] = sp[i];
+  ctx->n_listed = total;
+  ctx->max_row = flags[1];
+
+  // fused-kernel tiling and workspace
+  const int T = std::max(1, std::min(kTileMax, kEntCap / std::max(1, ctx->max_row)));
+  ctx->tile_atoms = T;
+  int64_t tiles = 0;
+  for (int sp_i = 0; sp_i < C; ++sp_i) tiles += (int64_t(sp[sp_i + 1] - sp[sp_i]) + T - 1) / T;
+  ctx->n_tiles = tiles;
+  ctx->n_blocks = int(std::max<int64_t>(1, std::min<int64_t>(tiles, ctx->n_cu)));
+  const int64_t chunks = std::min<int64_t>(kChunkCap, (int64_t(T) * ctx->max_row + 15) / 16 + C);
+  const size_t slot = size_t(chunks) * 2 * size_t(ctx->hp.k) * 16;
+  MLIP_TRY(ensure(ctx, &ctx->d_ws, &ctx->cap_ws, slot * size_t(ctx->n_blocks), "workspace"));
+  ctx->built = true;
+  ctx->n_builds += 1;
+  return MLIP_OK;
+}
+
+mlip_status mlip_compute(mlip_ctx* ctx, const double* pos_dev, double* energy_dev, double* forces_dev,
+                         double* virial_dev, double* totals_host) {
+  if (!ctx) return MLIP_E_ARG;
+  ctx->err.clear();
+  if (!pos_dev || !forces_dev) return fail(ctx, MLIP_E_ARG, "NULL positions or forces");
+  if (!ctx->built) return fail(ctx, MLIP_E_STATE, "mlip_build_neighbors has not been called");
+  hipStream_t s = ctx->stream;
+  const int64_t n = ctx->n;
+  MLIP_HIP(ctx, launch_fill_f64(forces_dev, 3 * n, 0.0, s));
+  MLIP_HIP(ctx, launch_fill_f64(ctx->d_totals, 16, 0.0, s));
+  MLIP_HIP(ctx, launch_fill_u64(ctx->d_counters, 4, s));
+
+  FusedArgs a{};
+  a.pos = pos_dev;
+  a.types = ctx->d_types;
+  a.perm = ctx->d_perm;
+  a.offsets = ctx->d_offsets;
+  a.idx = ctx->d_idx;
+  a.enc = ctx->d_enc;
+  a.head = ctx->d_head;
+  a.qc = ctx->d_qc;
+  a.energy = energy_dev;
+  a.forces = forces_dev;
+  a.virial = virial_dev;
+  a.totals = ctx->d_totals;
+  a.counters = ctx->d_counters;
+  a.ws = ctx->d_ws;
+  a.ws_slot = (long long)(ctx->cap_ws / size_t(ctx->n_blocks));
+  for (int d = 0; d < 3; ++d) {
+    a.box[d] = ctx->box[d];
+    a.inv_box[d] = 1.0 / ctx->box[d];
+  }
+  a.rc = ctx->hp.cutoff;
+  a.rc2 = ctx->hp.cutoff * ctx->hp.cutoff;
+  a.enc_stride = (long long)ctx->enc_stride;
+  a.head_stride = (long long)ctx->head_stride;
+  a.C = ctx->hp.n_species;
+  a.enc_cond = ctx->hp.enc_cond;
+  a.reg_cond = ctx->hp.reg_cond;
+  a.lmax = ctx->hp.lmax;
+  a.enc_hidden = ctx->hp.enc_hidden;
+  a.reg_hidden = ctx->hp.reg_hidden;
+  a.tile_atoms = ctx->tile_atoms;
+  a.n_tiles = int(ctx->n_tiles);
+  int t = 0;
+  for (int sp_i = 0; sp_i <= a.C; ++sp_i) {
+    a.species_start[sp_i] = ctx->species_start[sp_i];
+    a.tile_start[sp_i] = t;
+    if (sp_i < a.C) t += (ctx->species_start[sp_i + 1] - ctx->species_start[sp_i] + ctx->tile_atoms - 1) / ctx->tile_atoms;
+  }
+  if (ctx->n_tiles > 0) MLIP_HIP(ctx, launch_fused(ctx->hp.k, a, ctx->n_blocks, s));
+  if (totals_host) {
+    MLIP_HIP(ctx, hipMemcpyAsync(totals_host, ctx->d_totals, 10 * sizeof(double), hipMemcpyDeviceToHost, s));
+    MLIP_HIP(ctx, hipStreamSynchronize(s));
+  }
+  return MLIP_OK;
+}
+
+mlip_status mlip_get_neighbors(mlip_ctx* ctx, int64_t* offsets_host, int32_t* idx_host) {
+  if (!ctx) return MLIP_E_ARG;
+  if (!offsets_host || !idx_host) return fail(ctx, MLIP_E_ARG, "NULL argument");
+  if (!ctx->built) return fail(ctx, MLIP_E_STATE, "no neighbour list");
+  const int64_t n = ctx->n;
+  std::vector<int64_t> off(size_t(n + 1));
+  std::vector<int32_t> perm(static_cast<size_t>(n));
+  std::vector<int32_t> idx(static_cast<size_t>(std::max<int64_t>(ctx->n_listed, 1)));
+  MLIP_HIP(ctx, hipStreamSynchronize(ctx->stream));
+  MLIP_HIP(ctx, hipMemcpy(off.data(), ctx->d_offsets, off.size() * sizeof(int64_t), hipMemcpyDeviceToHost));
+  MLIP_HIP(ctx, hipMemcpy(perm.data(), ctx->d_perm, perm.size() * sizeof(int32_t), hipMemcpyDeviceToHost));
+  if (ctx->n_listed > 0)
+    MLIP_HIP(ctx, hipMemcpy(idx.data(), ctx->d_idx, size_t(ctx->n_listed) * sizeof(int32_t), hipMemcpyDeviceToHost));
+  std::vector<int64_t> len(size_t(n), 0);
+  for (int64_t a = 0; a < n; ++a) len[size_t(perm[size_t(a)])] = off[size_t(a + 1)] - off[size_t(a)];
+  offsets_host[0] = 0;
+  for (int64_t i = 0; i < n; ++i) offsets_host[i + 1] = offsets_host[i] + len[size_t(i)];
+  for (int64_t a = 0; a < n; ++a) {
+    const int64_t i = perm[size_t(a)];
+    std::memcpy(idx_host + offsets_host[i], idx.data() + off[size_t(a)], size_t(len[size_t(i)]) * sizeof(int32_t));
+  }
+  return MLIP_OK;
+}
+
+mlip_status mlip_memory_bytes(const mlip_ctx* ctx, size_t* bytes) {
+  if (!ctx || !bytes) return MLIP_E_ARG;
+  *bytes = ctx->bytes;
+  return MLIP_OK;
+}
+
+mlip_status mlip_get_stats(mlip_ctx* ctx, mlip_stats* st) {
+  if (!ctx || !st) return MLIP_E_ARG;
+  std::memset(st, 0, sizeof(*st));
+  unsigned long long active = 0;
+  if (ctx->d_counters) {
+    MLIP_HIP(ctx, hipMemcpyAsync(&active, ctx->d_counters, sizeof(active), hipMemcpyDeviceToHost, ctx->stream));
+    MLIP_HIP(ctx, hipStreamSynchronize(ctx->stream));
+  }
+  st->n_atoms = ctx->n;
+  st->n_listed_pairs = ctx->n_listed;
+  st->n_active_pairs = int64_t(active);
+  st->max_row = ctx->max_row;
+  st->tile_atoms = ctx->tile_atoms;
+  st->n_tiles = ctx->n_tiles;
+  st->n_blocks = ctx->n_blocks;
+  st->n_cells = ctx->grid.ncell;
+  st->n_builds = ctx->n_builds;
+  st->device_bytes = ctx->bytes;
+  return MLIP_OK;
+}
+
+const char* mlip_last_error(const mlip_ctx* ctx) {
+  if (!ctx) return "invalid context";
+  return ctx->err.c_str();
+}
+
+void mlip_destroy(mlip_ctx* ctx) {
+  if (!ctx) return;
+  (void)hipDeviceSynchronize();
+  void* bufs[] = {ctx->d_enc, ctx->d_head, ctx->d_qc, ctx->d_inv_mass, ctx->d_types, ctx->d_perm,
+                  ctx->d_key, ctx->d_spos, ctx->d_rowcnt, ctx->d_offsets, ctx->d_idx, ctx->d_cell_count,
+                  ctx->d_cell_start, ctx->d_scan_tmp, ctx->d_ws, ctx->d_totals, ctx->d_counters,
+                  ctx->d_flags, ctx->d_reduce};
+  for (void* p : bufs)
+    if (p) (void)hipFree(p);
+  (void)hipGetLastError();
+  delete ctx;
+}
+
+mlip_status mlip_md_set_masses(mlip_ctx* ctx, const double* masses_host) {
+  if (!ctx) return MLIP_E_ARG;
+  if (!masses_host) return fail(ctx, MLIP_E_ARG, "NULL masses");
+  double inv[kMaxSpecies] = {0};
+  for (int s = 0; s < ctx->hp.n_species; ++s) {
+    if (!(masses_host[s] > 0.0) || !std::isfinite(masses_host[s])) return fail(ctx, MLIP_E_ARG, "masses must be positive");
+    inv[s] = kAccPerForceMass / masses_host[s];
+  }
+  MLIP_HIP(ctx, hipMemcpyAsync(ctx->d_inv_mass, inv, sizeof(inv), hipMemcpyHostToDevice, ctx->stream));
+  MLIP_HIP(ctx, hipStreamSynchronize(ctx->stream));
+  ctx->masses_set = true;
+  return MLIP_OK;
+}
+
+mlip_status mlip_md_first_half(mlip_ctx* ctx, double* pos_dev, double* vel_dev, const double* forces_dev, double dt,
+                               const double* ref_dev, double* max_disp2_host) {
+  if (!ctx) return MLIP_E_ARG;
+  if (!pos_dev || !vel_dev || !forces_dev) return fail(ctx, MLIP_E_ARG, "NULL argument");
+  if (!ctx->built || !ctx->masses_set) return fail(ctx, MLIP_E_STATE, "build neighbours and set masses first");
+  const bool track = ref_dev && max_disp2_host;
+  if (track) MLIP_HIP(ctx, launch_fill_f64(ctx->d_reduce, 1, 0.0, ctx->stream));
+  MLIP_HIP(ctx, launch_md_first_half(pos_dev, vel_dev, forces_dev, ctx->d_types, ctx->d_inv_mass, ctx->n, dt,
+                                     track ? ref_dev : nullptr, ctx->d_reduce, ctx->stream));
+  if (track) {
+    MLIP_HIP(ctx, hipMemcpyAsync(max_disp2_host, ctx->d_reduce, sizeof(double), hipMemcpyDeviceToHost, ctx->stream));
+    MLIP_HIP(ctx, hipStreamSynchronize(ctx->stream));
+  }
+  return MLIP_OK;
+}
+
+mlip_status mlip_md_second_half(mlip_ctx* ctx, double* vel_dev, const double* forces_dev, double dt) {
+  if (!ctx) return MLIP_E_ARG;
+  if (!vel_dev || !forces_dev) return fail(ctx, MLIP_E_ARG, "NULL argument");
+  if (!ctx->built || !ctx->masses_set) return fail(ctx, MLIP_E_STATE, "build neighbours and set masses first");
+  MLIP_HIP(ctx, launch_md_second_half(vel_dev, forces_dev, ctx->d_types, ctx->d_inv_mass, ctx->n, dt, ctx->stream));
+  return MLIP_OK;
+}
+
+mlip_status mlip_md_kinetic(mlip_ctx* ctx, const double* vel_dev, double* ke_host) {
+  if (!ctx) return MLIP_E_ARG;
+  if (!vel_dev || !ke_host) return fail(ctx, MLIP_E_ARG, "NULL argument");
+  if (!ctx->built || !ctx->masses_set) return fail(ctx, MLIP_E_STATE, "build neighbours and set masses first");
+  MLIP_HIP(ctx, launch_fill_f64(ctx->d_reduce + 1, 1, 0.0, ctx->stream));
+  MLIP_HIP(ctx, launch_md_kinetic(vel_dev, ctx->d_types, ctx->d_inv_mass, ctx->n, ctx->d_reduce + 1, ctx->stream));
+  MLIP_HIP(ctx, hipMemcpyAsync(ke_host, ctx->d_reduce + 1, sizeof(double), hipMemcpyDeviceToHost, ctx->stream));
+  MLIP_HIP(ctx, hipStreamSynchronize(ctx->stream));
+  return MLIP_OK;
+}
+
+}  // extern "C"

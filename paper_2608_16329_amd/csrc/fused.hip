@@ -1,0 +1,700 @@
+// Fused energy / force / virial kernel for gfx950 (Section 3.1, Eqs. 1-10;
+// fusion as in Section 3.4, re-designed for CDNA4).
+//
+// One persistent work-group (4 wavefronts, one per SIMD) walks a list of
+// tiles.  A tile is up to 16 centre atoms of one species, consecutive in the
+// cell-sorted order.  Per tile:
+//
+//   A. Stage the tile's atoms and neighbour rows; keep pairs with r < r_c and
+//      bucket them by neighbour species in LDS, in atom order.  Each bucket
+//      is cut into 16-pair chunks; all pairs of a chunk share one encoder
+//      table (pair conditioning, Section 3.2).
+//   B. Pass 1, one chunk per wavefront at a time: the radial encoder (Eq. 2)
+//      and its derivative in r run as float64 MFMA 16x16x4 products with the
+//      16 pairs as one matrix dimension, the activation and its tangent
+//      stacked as two column tiles sharing every weight fragment.  The
+//      moment P_i = sum_j g_ang (x) g_rad (Eq. 4) is another MFMA product
+//      (K = pairs), accumulated into LDS.  The pre-cutoff output m and its
+//      tangent dm (2k doubles per pair) go to a fixed-size per-work-group
+//      workspace; nothing is recomputed in pass 2.
+//   C. Descriptor (Eq. 5), energy head (Eq. 6) and its gradient, and
+//      W_i = dE_i/dP_i (Eq. 7) for the tile's atoms, in LDS (W overwrites P).
+//   D. Pass 2, per chunk: v = W g and the reassociated radial term
+//      s = g_ang^T W g' (Eqs. 8-9; U_i is never formed) as MFMA products,
+//      then f_ij (Eq. 10), scatter F_j -= f_ij (global atomics) and
+//      F_i += f_ij, w_i -= r_ij (x) f_ij (LDS atomics).
+//   E. Write E_i, w_i, add F_i; block-reduce totals.
+//
+// MFMA f64 16x16x4 register layout on gfx950 (lane = 16*g + c):
+//   A operand: lane holds A[c][g]; B operand: lane holds B[g][c];
+//   D/C: register q of lane holds D[4q + g][c].
+// A D-tile X can therefore feed a later product as B (contracting over its
+// rows, k-step q covers rows 4q..4q+3) or as A (X^T, same contraction).
+#include "mlip_internal.h"
+
+namespace mlip {
+namespace {
+
+typedef double v4d __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ v4d mfma(double a, double b, v4d c) {
+  return __builtin_amdgcn_mfma_f64_16x16x4f64(a, b, c, 0, 0, 0);
+}
+
+__device__ __forceinline__ double sigmoid(double z) { return 1.0 / (1.0 + exp(-z)); }
+
+__device__ __forceinline__ double fold(double d, double L, double invL) { return d - L * rint(d * invL); }
+
+// Cartesian monomials of degree <= 3 in the order of the angular table.
+__device__ __forceinline__ void monomials(double x, double y, double z, double m[kMonomials]) {
+  m[0] = 1.0;
+  m[1] = x; m[2] = y; m[3] = z;
+  m[4] = x * x; m[5] = x * y; m[6] = x * z; m[7] = y * y; m[8] = y * z; m[9] = z * z;
+  m[10] = x * x * x; m[11] = x * x * y; m[12] = x * x * z; m[13] = x * y * y; m[14] = x * y * z;
+  m[15] = x * z * z; m[16] = y * y * y; m[17] = y * y * z; m[18] = y * z * z; m[19] = z * z * z;
+}
+
+// Gradients of the monomials with respect to (x, y, z).
+__device__ __forceinline__ void monomial_grads(double x, double y, double z, double gx[kMonomials],
+                                               double gy[kMonomials], double gz[kMonomials]) {
+  const double xx = x * x, yy = y * y, zz = z * z;
+  gx[0] = 0; gy[0] = 0; gz[0] = 0;
+  gx[1] = 1; gy[1] = 0; gz[1] = 0;
+  gx[2] = 0; gy[2] = 1; gz[2] = 0;
+  gx[3] = 0; gy[3] = 0; gz[3] = 1;
+  gx[4] = 2 * x; gy[4] = 0; gz[4] = 0;
+  gx[5] = y; gy[5] = x; gz[5] = 0;
+  gx[6] = z; gy[6] = 0; gz[6] = x;
+  gx[7] = 0; gy[7] = 2 * y; gz[7] = 0;
+  gx[8] = 0; gy[8] = z; gz[8] = y;
+  gx[9] = 0; gy[9] = 0; gz[9] = 2 * z;
+  gx[10] = 3 * xx; gy[10] = 0; gz[10] = 0;
+  gx[11] = 2 * x * y; gy[11] = xx; gz[11] = 0;
+  gx[12] = 2 * x * z; gy[12] = 0; gz[12] = xx;
+  gx[13] = yy; gy[13] = 2 * x * y; gz[13] = 0;
+  gx[14] = y * z; gy[14] = x * z; gz[14] = x * y;
+  gx[15] = zz; gy[15] = 0; gz[15] = 2 * x * z;
+  gx[16] = 0; gy[16] = 3 * yy; gz[16] = 0;
+  gx[17] = 0; gy[17] = 2 * y * z; gz[17] = yy;
+  gx[18] = 0; gy[18] = zz; gz[18] = 2 * y * z;
+  gx[19] = 0; gy[19] = 0; gz[19] = 3 * zz;
+}
+
+template <int K, int TM>
+struct Smem {
+  double P[TM][kAngRows][K + 1];  // moment, then its adjoint W (padded rows)
+  double x[TM][4 * K];            // head input vec(G)
+  double ybuf[TM][kHeadWidth];
+  double gbuf[TM][kHeadWidth];
+  double qc[kAngRows][kMonomials];
+  double tpos[TM][3];
+  double Fi[TM][3];
+  double Wi[TM][9];
+  double Ei[TM];
+  long long row_beg[TM];
+  int row_len[TM];
+  int ent_base[TM + 1];
+  int orig[TM];
+  int cnt[kMaxSpecies][TM];
+  int base[kMaxSpecies][TM];
+  int ent_j[kEntCap];
+  int pair_j[kEntCap];
+  signed char ent_s[kEntCap];
+  unsigned char pair_a[kEntCap];
+  int ch_start[kChunkCap];
+  unsigned char ch_count[kChunkCap];
+  unsigned char ch_s[kChunkCap];
+  int n_chunks;
+  int n_active;
+  int tile_species;
+  int na;
+};
+
+// Pass 1 on one chunk: encoder forward + tangent, moment accumulation and
+// the workspace write of (m, dm).
+template <int K, int TM>
+__device__ void pass1_chunk(const FusedArgs& A, Smem<K, TM>& S, int ch, double* __restrict__ wsc) {
+  constexpr int KT = K / 16;
+  const int lane = threadIdx.x & 63, g = lane >> 4, c = lane & 15;
+  const int start = S.ch_start[ch], count = S.ch_count[ch];
+  const int sj = S.ch_s[ch], si = S.tile_species;
+  const int tau = A.enc_cond == 2 ? si * A.C + sj : (A.enc_cond == 1 ? sj : 0);
+  const double* __restrict__ tab = A.enc + (long long)tau * A.enc_stride;
+
+  // geometry of the pair in column c (Eq. 1)
+  const bool valid = c < count;
+  double ux = 1.0, uy = 0.0, uz = 0.0, r = 1.0, fc = 0.0;
+  int atom = -1;
+  if (valid) {
+    const int e = start + c;
+    const int j = S.pair_j[e];
+    atom = S.pair_a[e];
+    const double dx = fold(A.pos[3 * (long long)j] - S.tpos[atom][0], A.box[0], A.inv_box[0]);
+    const double dy = fold(A.pos[3 * (long long)j + 1] - S.tpos[atom][1], A.box[1], A.inv_box[1]);
+    const double dz = fold(A.pos[3 * (long long)j + 2] - S.tpos[atom][2], A.box[2], A.inv_box[2]);
+    r = sqrt(dx * dx + dy * dy + dz * dz);
+    const double ir = 1.0 / r;
+    ux = dx * ir; uy = dy * ir; uz = dz * ir;
+    fc = 0.5 * (1.0 + cos(M_PI * r / A.rc));
+  }
+
+  // first layer (scalar input), rows in = 16T + 4i + g of column c
+  double h[8][4], dh[8][4];
+#pragma unroll
+  for (int T = 0; T < 8; ++T)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int in = 16 * T + 4 * i + g;
+      const double w0 = tab[in], z = w0 * r + tab[kEncWidth + in];
+      const double s = sigmoid(z);
+      h[T][i] = z * s;
+      dh[T][i] = s * (1.0 + z * (1.0 - s)) * w0;
+    }
+
+  // residual hidden layers: Z = W H as 8 x 32 MFMA steps, forward and
+  // tangent columns share each weight fragment
+  const double* __restrict__ layer = tab + 2 * kEncWidth;
+  for (int t = 1; t < A.enc_hidden; ++t) {
+    const double* __restrict__ frag = layer + lane;
+    const double* __restrict__ bias = layer + kEncWidth * kEncWidth;
+    v4d acc[8], dacc[8];
+#pragma unroll
+    for (int To = 0; To < 8; ++To) {
+      acc[To] = v4d{0, 0, 0, 0};
+      dacc[To] = v4d{0, 0, 0, 0};
+    }
+#pragma unroll
+    for (int T = 0; T < 8; ++T)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        double w[8];
+#pragma unroll
+        for (int To = 0; To < 8; ++To) w[To] = frag[((T * 4 + i) * 8 + To) * 64];
+#pragma unroll
+        for (int To = 0; To < 8; ++To) {
+          acc[To] = mfma(w[To], h[T][i], acc[To]);
+          dacc[To] = mfma(w[To], dh[T][i], dacc[To]);
+        }
+      }
+#pragma unroll
+    for (int To = 0; To < 8; ++To)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const double z = acc[To][q] + bias[16 * To + 4 * q + g];
+        const double s = sigmoid(z);
+        h[To][q] += z * s;
+        dh[To][q] += s * (1.0 + z * (1.0 - s)) * dacc[To][q];
+      }
+    layer += kEncWidth * kEncWidth + kEncWidth;
+  }
+
+  // output layer with pairs as rows: m[pair 4q+g][16Tc + c]
+  v4d mo[KT], dmo[KT];
+#pragma unroll
+  for (int Tc = 0; Tc < KT; ++Tc) {
+    mo[Tc] = v4d{0, 0, 0, 0};
+    dmo[Tc] = v4d{0, 0, 0, 0};
+  }
+  {
+    const double* __restrict__ frag = layer + lane;
+#pragma unroll
+    for (int T = 0; T < 8; ++T)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        double w[KT];
+#pragma unroll
+        for (int Tc = 0; Tc < KT; ++Tc) w[Tc] = frag[((T * 4 + i) * KT + Tc) * 64];
+#pragma unroll
+        for (int Tc = 0; Tc < KT; ++Tc) {
+          mo[Tc] = mfma(h[T][i], w[Tc], mo[Tc]);
+          dmo[Tc] = mfma(dh[T][i], w[Tc], dmo[Tc]);
+        }
+      }
+    const double* __restrict__ bout = layer + K * kEncWidth;
+#pragma unroll
+    for (int Tc = 0; Tc < KT; ++Tc) {
+      const double b = bout[16 * Tc + c];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) mo[Tc][q] += b;
+    }
+  }
+
+  // moment: P[mm][col] += sum_pairs fc * a_mm(u) * m[pair][col], one MFMA
+  // product per centre atom present in the chunk (pairs of other atoms are
+  // masked to zero in the A operand)
+  double av[4];
+  int aa[4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int src = 4 * q + g;  // pair index; any lane with c == src holds it
+    const double px = __shfl(ux, src, 64), py = __shfl(uy, src, 64), pz = __shfl(uz, src, 64);
+    const double pf = __shfl(fc, src, 64);
+    aa[q] = __shfl(atom, src, 64);
+    double mono[kMonomials];
+    monomials(px, py, pz, mono);
+    double s = 0.0;
+#pragma unroll
+    for (int m = 0; m < kMonomials; ++m) s += S.qc[c][m] * mono[m];
+    av[q] = pf * s;
+  }
+  const int a_first = S.pair_a[start], a_last = S.pair_a[start + count - 1];
+  for (int a = a_first; a <= a_last; ++a) {
+    v4d pacc[KT];
+#pragma unroll
+    for (int Tc = 0; Tc < KT; ++Tc) pacc[Tc] = v4d{0, 0, 0, 0};
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const double av_a = aa[q] == a ? av[q] : 0.0;
+#pragma unroll
+      for (int Tc = 0; Tc < KT; ++Tc) pacc[Tc] = mfma(av_a, mo[Tc][q], pacc[Tc]);
+    }
+#pragma unroll
+    for (int Tc = 0; Tc < KT; ++Tc)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) atomicAdd(&S.P[a][4 * q + g][16 * Tc + c], pacc[Tc][q]);
+  }
+
+  // workspace in the B-operand layout pass 2 loads: block (Tc, i) holds
+  // m[c' = 16Tc + 4i + g'][pair c'] at lane 16 g' + c'
+#pragma unroll
+  for (int Tc = 0; Tc < KT; ++Tc)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int off = (Tc * 4 + (c >> 2)) * 64 + 16 * (c & 3) + 4 * q + g;
+      wsc[off] = mo[Tc][q];
+      wsc[K * 16 + off] = dmo[Tc][q];
+    }
+}
+
+// Pass 2 on one chunk: W contractions, partial forces and scatter.
+template <int K, int TM>
+__device__ void pass2_chunk(const FusedArgs& A, Smem<K, TM>& S, int ch, const double* __restrict__ wsc) {
+  constexpr int KT = K / 16;
+  const int lane = threadIdx.x & 63, g = lane >> 4, c = lane & 15;
+  const int start = S.ch_start[ch], count = S.ch_count[ch];
+
+  double mB[KT][4], dmB[KT][4];
+#pragma unroll
+  for (int Tc = 0; Tc < KT; ++Tc)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      mB[Tc][i] = wsc[(Tc * 4 + i) * 64 + lane];
+      dmB[Tc][i] = wsc[K * 16 + (Tc * 4 + i) * 64 + lane];
+    }
+
+  const bool valid = c < count;
+  int atom = -1, j = 0;
+  double dx = 1.0, dy = 0.0, dz = 0.0, r = 1.0;
+  if (valid) {
+    const int e = start + c;
+    j = S.pair_j[e];
+    atom = S.pair_a[e];
+    dx = fold(A.pos[3 * (long long)j] - S.tpos[atom][0], A.box[0], A.inv_box[0]);
+    dy = fold(A.pos[3 * (long long)j + 1] - S.tpos[atom][1], A.box[1], A.inv_box[1]);
+    dz = fold(A.pos[3 * (long long)j + 2] - S.tpos[atom][2], A.box[2], A.inv_box[2]);
+    r = sqrt(dx * dx + dy * dy + dz * dz);
+  }
+  const double ir = 1.0 / r;
+  const double ux = dx * ir, uy = dy * ir, uz = dz * ir;
+  const double arg = M_PI * r / A.rc;
+  const double fc = valid ? 0.5 * (1.0 + cos(arg)) : 0.0;
+  const double dfc = valid ? -0.5 * M_PI / A.rc * sin(arg) : 0.0;
+
+  // (W m) and (W dm) for this column's own centre atom
+  v4d wm = v4d{0, 0, 0, 0}, wdm = v4d{0, 0, 0, 0};
+  const int a_first = S.pair_a[start], a_last = S.pair_a[start + count - 1];
+  for (int a = a_first; a <= a_last; ++a) {
+    v4d t1 = v4d{0, 0, 0, 0}, t2 = v4d{0, 0, 0, 0};
+#pragma unroll
+    for (int Tc = 0; Tc < KT; ++Tc)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const double w = S.P[a][c][16 * Tc + 4 * i + g];
+        t1 = mfma(w, mB[Tc][i], t1);
+        t2 = mfma(w, dmB[Tc][i], t2);
+      }
+    if (atom == a) {
+      wm = t1;
+      wdm = t2;
+    }
+  }
+
+  // angular features a_mm and gradients for rows mm = 4q + g of this pair
+  double mono[kMonomials], gx[kMonomials], gy[kMonomials], gz[kMonomials];
+  monomials(ux, uy, uz, mono);
+  monomial_grads(ux, uy, uz, gx, gy, gz);
+  double s = 0.0, tx = 0.0, ty = 0.0, tz = 0.0;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int mm = 4 * q + g;
+    double a_v = 0.0, a_x = 0.0, a_y = 0.0, a_z = 0.0;
+#pragma unroll
+    for (int m = 0; m < kMonomials; ++m) {
+      const double co = S.qc[mm][m];
+      a_v += co * mono[m];
+      a_x += co * gx[m];
+      a_y += co * gy[m];
+      a_z += co * gz[m];
+    }
+    const double v = fc * wm[q];                      // v = W g
+    const double wg = dfc * wm[q] + fc * wdm[q];      // W g'
+    s += a_v * wg;
+    tx += a_x * v;
+    ty += a_y * v;
+    tz += a_z * v;
+  }
+#pragma unroll
+  for (int o = 16; o <= 32; o <<= 1) {
+    s += __shfl_xor(s, o, 64);
+    tx += __shfl_xor(tx, o, 64);
+    ty += __shfl_xor(ty, o, 64);
+    tz += __shfl_xor(tz, o, 64);
+  }
+  // f = s u + (I - u u^T) t / r  (Eq. 10, reassociated)
+  const double ut = ux * tx + uy * ty + uz * tz;
+  const double fx = s * ux + (tx - ut * ux) * ir;
+  const double fy = s * uy + (ty - ut * uy) * ir;
+  const double fz = s * uz + (tz - ut * uz) * ir;
+  if (valid) {
+    if (g == 0) {
+      atomicAdd(&A.forces[3 * (long long)j], -fx);
+      atomicAdd(&A.forces[3 * (long long)j + 1], -fy);
+      atomicAdd(&A.forces[3 * (long long)j + 2], -fz);
+    } else if (g == 1) {
+      atomicAdd(&S.Fi[atom][0], fx);
+      atomicAdd(&S.Fi[atom][1], fy);
+      atomicAdd(&S.Fi[atom][2], fz);
+    } else if (g == 2) {
+      atomicAdd(&S.Wi[atom][0], -dx * fx);
+      atomicAdd(&S.Wi[atom][1], -dx * fy);
+      atomicAdd(&S.Wi[atom][2], -dx * fz);
+      atomicAdd(&S.Wi[atom][3], -dy * fx);
+      atomicAdd(&S.Wi[atom][4], -dy * fy);
+    } else {
+      atomicAdd(&S.Wi[atom][5], -dy * fz);
+      atomicAdd(&S.Wi[atom][6], -dz * fx);
+      atomicAdd(&S.Wi[atom][7], -dz * fy);
+      atomicAdd(&S.Wi[atom][8], -dz * fz);
+    }
+  }
+}
+
+// Descriptor, head forward/backward and W for the tile (all threads).
+template <int K, int TM>
+__device__ void head_stage(const FusedArgs& A, Smem<K, TM>& S) {
+  const int tid = threadIdx.x;
+  const int na = S.na;
+  const int nin = (A.lmax + 1) * K;
+  // Eq. 5: G[0,c] = P[0,c]; G[l,c] = sum over the order-l rows of P^2
+  for (int u = tid; u < na * K; u += kThreads) {
+    const int a = u / K, c = u % K;
+    S.x[a][c] = S.P[a][0][c];
+    for (int l = 1; l <= A.lmax; ++l) {
+      double sq = 0.0;
+      for (int mm = l * l; mm < (l + 1) * (l + 1); ++mm) sq += S.P[a][mm][c] * S.P[a][mm][c];
+      S.x[a][l * K + c] = sq;
+    }
+  }
+  __syncthreads();
+
+  const int rho = A.reg_cond ? S.tile_species : 0;
+  const double* __restrict__ ht = A.head + (long long)rho * A.head_stride;
+  const double* __restrict__ A0T = ht;                          // [nin][64]
+  const double* __restrict__ A0 = ht + kHeadWidth * nin;        // [64][nin]
+  const double* __restrict__ c0 = A0 + kHeadWidth * nin;
+  const double* __restrict__ hid = c0 + kHeadWidth;
+  const int a = tid >> 4, o4 = tid & 15;
+  const bool act = a < na;
+  double zeta[kMaxHidden][4];
+
+  // Eq. 6 forward
+  if (act) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int o = o4 + 16 * q;
+      double z = c0[o];
+      for (int in = 0; in < nin; ++in) z += A0T[in * kHeadWidth + o] * S.x[a][in];
+      zeta[0][q] = z;
+      S.ybuf[a][o] = z * sigmoid(z);
+    }
+  }
+  __syncthreads();
+#pragma unroll
+  for (int t = 1; t < kMaxHidden; ++t) {
+    if (t >= A.reg_hidden) break;
+    const double* __restrict__ AtT = hid + (t - 1) * (2 * kHeadWidth * kHeadWidth + kHeadWidth);
+    const double* __restrict__ ct = AtT + 2 * kHeadWidth * kHeadWidth;
+    double z[4] = {0, 0, 0, 0};
+    if (act) {
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int o = o4 + 16 * q;
+        double acc = ct[o];
+        for (int in = 0; in < kHeadWidth; ++in) acc += AtT[in * kHeadWidth + o] * S.ybuf[a][in];
+        z[q] = acc;
+        zeta[t][q] = acc;
+      }
+    }
+    __syncthreads();
+    if (act) {
+#pragma unroll
+      for (int q = 0; q < 4; ++q) S.ybuf[a][o4 + 16 * q] += z[q] * sigmoid(z[q]);
+    }
+    __syncthreads();
+  }
+  const double* __restrict__ aout = hid + (A.reg_hidden - 1) * (2 * kHeadWidth * kHeadWidth + kHeadWidth);
+  const double cout = aout[kHeadWidth];
+  double part = 0.0;
+  double d[4];
+  if (act) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      part += aout[o4 + 16 * q] * S.ybuf[a][o4 + 16 * q];
+      d[q] = aout[o4 + 16 * q];
+    }
+  }
+#pragma unroll
+  for (int o = 1; o < 16; o <<= 1) part += __shfl_xor(part, o, 64);
+  if (act && o4 == 0) S.Ei[a] = part + cout;
+
+  // backward through the residual layers: d <- d + A_t^T (silu'(zeta_t) d)
+#pragma unroll
+  for (int t = kMaxHidden - 1; t >= 1; --t) {
+    if (t >= A.reg_hidden) continue;
+    const double* __restrict__ At = hid + (t - 1) * (2 * kHeadWidth * kHeadWidth + kHeadWidth) +
+                                    kHeadWidth * kHeadWidth;  // [64][64] row-major [out][in]
+    if (act) {
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const double z = zeta[t][q], s = sigmoid(z);
+        S.gbuf[a][o4 + 16 * q] = s * (1.0 + z * (1.0 - s)) * d[q];
+      }
+    }
+    __syncthreads();
+    if (act) {
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int in = o4 + 16 * q;
+        double acc = 0.0;
+        for (int o = 0; o < kHeadWidth; ++o) acc += At[o * kHeadWidth + in] * S.gbuf[a][o];
+        d[q] += acc;
+      }
+    }
+    __syncthreads();
+  }
+  if (act) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const double z = zeta[0][q], s = sigmoid(z);
+      S.gbuf[a][o4 + 16 * q] = s * (1.0 + z * (1.0 - s)) * d[q];
+    }
+  }
+  __syncthreads();
+  // dE/dx = A0^T (silu'(zeta0) d), then Eq. 7: W = dE/dP in place of P
+  if (act) {
+    for (int in = o4; in < nin; in += 16) {
+      double acc = 0.0;
+      for (int o = 0; o < kHeadWidth; ++o) acc += A0[o * nin + in] * S.gbuf[a][o];
+      const int l = in / K, c = in % K;
+      if (l == 0) {
+        S.P[a][0][c] = acc;
+      } else {
+        for (int mm = l * l; mm < (l + 1) * (l + 1); ++mm) S.P[a][mm][c] *= 2.0 * acc;
+      }
+    }
+  }
+  __syncthreads();
+}
+
+template <int K, int TM>
+__global__ __launch_bounds__(kThreads, 1) void k_fused(FusedArgs A) {
+  extern __shared__ __align__(16) unsigned char smem_raw[];
+  Smem<K, TM>& S = *reinterpret_cast<Smem<K, TM>*>(smem_raw);
+  const int tid = threadIdx.x, wave = tid >> 6;
+  constexpr int KT = K / 16;
+  const long long chunk_doubles = 2LL * K * 16;
+  double* __restrict__ ws_slot = A.ws + (long long)blockIdx.x * A.ws_slot;
+
+  for (int u = tid; u < kAngRows * kMonomials; u += kThreads) S.qc[u / kMonomials][u % kMonomials] = A.qc[u];
+
+  // XCD-aware assignment: blocks are dispatched round-robin over the 8 XCDs,
+  // so block b works on the b%8-th contiguous eighth of the tile list and
+  // spatially adjacent tiles share an L2.
+  const int G = gridDim.x;
+  const int nx = (G % 8 == 0) ? 8 : 1;
+  const int xcd = blockIdx.x % nx, slot = blockIdx.x / nx, per = G / nx;
+  const int lo = int((long long)A.n_tiles * xcd / nx), hi = int((long long)A.n_tiles * (xcd + 1) / nx);
+
+  for (int tile = lo + slot; tile < hi; tile += per) {
+    // ---- A: stage atoms and rows -----------------------------------------
+    if (tid == 0) {
+      int s = 0;
+      while (s + 1 < A.C && tile >= A.tile_start[s + 1]) ++s;
+      const int a0 = A.species_start[s] + (tile - A.tile_start[s]) * A.tile_atoms;
+      const int rem = A.species_start[s + 1] - a0;
+      S.tile_species = s;
+      S.na = rem < A.tile_atoms ? rem : A.tile_atoms;
+      S.ent_base[0] = a0;  // temporarily the first sorted slot
+    }
+    __syncthreads();
+    const int na = S.na;
+    const int a0 = S.ent_base[0];
+    if (tid < TM) {
+      if (tid < na) {
+        const int o = A.perm[a0 + tid];
+        S.orig[tid] = o;
+        S.tpos[tid][0] = A.pos[3 * (long long)o];
+        S.tpos[tid][1] = A.pos[3 * (long long)o + 1];
+        S.tpos[tid][2] = A.pos[3 * (long long)o + 2];
+        const long long b = A.offsets[a0 + tid];
+        S.row_beg[tid] = b;
+        S.row_len[tid] = int(A.offsets[a0 + tid + 1] - b);
+      } else {
+        S.row_len[tid] = 0;
+      }
+#pragma unroll
+      for (int k = 0; k < 3; ++k) S.Fi[tid][k] = 0.0;
+#pragma unroll
+      for (int k = 0; k < 9; ++k) S.Wi[tid][k] = 0.0;
+      S.Ei[tid] = 0.0;
+    }
+    for (int u = tid; u < kMaxSpecies * TM; u += kThreads) S.cnt[u / TM][u % TM] = 0;
+    for (int u = tid; u < TM * kAngRows * (K + 1); u += kThreads) (&S.P[0][0][0])[u] = 0.0;
+    __syncthreads();
+    if (tid == 0) {
+      int e = 0;
+      for (int a = 0; a < TM; ++a) {
+        S.ent_base[a] = e;
+        e += S.row_len[a];
+      }
+      S.ent_base[TM] = e;
+    }
+    __syncthreads();
+    const int nent = S.ent_base[TM];
+    for (int e = tid; e < nent; e += kThreads) {
+      int a = 0;
+      while (a + 1 < na && e >= S.ent_base[a + 1]) ++a;
+      const int j = A.idx[S.row_beg[a] + (e - S.ent_base[a])];
+      const double dx = fold(A.pos[3 * (long long)j] - S.tpos[a][0], A.box[0], A.inv_box[0]);
+      const double dy = fold(A.pos[3 * (long long)j + 1] - S.tpos[a][1], A.box[1], A.inv_box[1]);
+      const double dz = fold(A.pos[3 * (long long)j + 2] - S.tpos[a][2], A.box[2], A.inv_box[2]);
+      const bool active = dx * dx + dy * dy + dz * dz < A.rc2;
+      const int s = A.types[j];
+      S.ent_j[e] = j;
+      S.ent_s[e] = active ? (signed char)s : (signed char)-1;
+      if (active) atomicAdd(&S.cnt[s][a], 1);
+    }
+    __syncthreads();
+    if (tid == 0) {
+      int run = 0, nch = 0;
+      for (int s = 0; s < A.C; ++s) {
+        const int b0 = run;
+        for (int a = 0; a < na; ++a) {
+          S.base[s][a] = run;
+          run += S.cnt[s][a];
+        }
+        for (int off = b0; off < run; off += 16) {
+          S.ch_start[nch] = off;
+          S.ch_count[nch] = (unsigned char)(run - off < 16 ? run - off : 16);
+          S.ch_s[nch] = (unsigned char)s;
+          ++nch;
+        }
+      }
+      S.n_chunks = nch;
+      S.n_active = run;
+    }
+    __syncthreads();
+    if (tid < na) {
+      int next[kMaxSpecies];
+      for (int s = 0; s < A.C; ++s) next[s] = S.base[s][tid];
+      const int e1 = S.ent_base[tid + 1];
+      for (int e = S.ent_base[tid]; e < e1; ++e) {
+        const int s = S.ent_s[e];
+        if (s >= 0) {
+          const int p = next[s]++;
+          S.pair_j[p] = S.ent_j[e];
+          S.pair_a[p] = (unsigned char)tid;
+        }
+      }
+    }
+    __syncthreads();
+
+    // ---- B: pass 1 ---------------------------------------------------------
+    const int nch = S.n_chunks;
+    for (int ch = wave; ch < nch; ch += kWaves) pass1_chunk<K, TM>(A, S, ch, ws_slot + ch * chunk_doubles);
+    __syncthreads();
+
+    // ---- C: descriptor, head, W ------------------------------------------
+    head_stage<K, TM>(A, S);
+
+    // ---- D: pass 2 ---------------------------------------------------------
+    for (int ch = wave; ch < nch; ch += kWaves) pass2_chunk<K, TM>(A, S, ch, ws_slot + ch * chunk_doubles);
+    __syncthreads();
+
+    // ---- E: outputs --------------------------------------------------------
+    if (tid < na) {
+      const long long o = S.orig[tid];
+      if (A.energy) A.energy[o] = S.Ei[tid];
+      if (A.virial) {
+#pragma unroll
+        for (int k = 0; k < 9; ++k) A.virial[9 * o + k] = S.Wi[tid][k];
+      }
+      atomicAdd(&A.forces[3 * o], S.Fi[tid][0]);
+      atomicAdd(&A.forces[3 * o + 1], S.Fi[tid][1]);
+      atomicAdd(&A.forces[3 * o + 2], S.Fi[tid][2]);
+    }
+    if (wave == 0) {
+      double v[10];
+      const bool own = tid < na;
+      v[0] = own ? S.Ei[tid] : 0.0;
+#pragma unroll
+      for (int k = 0; k < 9; ++k) v[1 + k] = own ? S.Wi[tid][k] : 0.0;
+#pragma unroll
+      for (int k = 0; k < 10; ++k)
+#pragma unroll
+        for (int o = 1; o < 64; o <<= 1) v[k] += __shfl_xor(v[k], o, 64);
+      if (tid < 10) {
+        double mine = v[0];
+#pragma unroll
+        for (int k = 1; k < 10; ++k)
+          if (tid == k) mine = v[k];
+        atomicAdd(&A.totals[tid], mine);
+      }
+      if (tid == 0) atomicAdd(&A.counters[0], (unsigned long long)S.n_active);
+    }
+    __syncthreads();
+    (void)KT;
+  }
+}
+
+template <int K, int TM>
+hipError_t launch_k(const FusedArgs& a, int n_blocks, hipStream_t s) {
+  const size_t smem = sizeof(Smem<K, TM>);
+  static bool attr_set = false;
+  if (!attr_set) {
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_fused<K, TM>),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, int(smem));
+    if (e != hipSuccess) return e;
+    attr_set = true;
+  }
+  k_fused<K, TM><<<dim3(unsigned(n_blocks)), dim3(kThreads), smem, s>>>(a);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+size_t fused_smem_bytes(int k) {
+  switch (k) {
+    case 32: return sizeof(Smem<32, kTileMax>);
+    default: return 0;
+  }
+}
+
+hipError_t launch_fused(int k, const FusedArgs& a, int n_blocks, hipStream_t s) {
+  switch (k) {
+    case 32: return launch_k<32, kTileMax>(a, n_blocks, s);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+}  // namespace mlip

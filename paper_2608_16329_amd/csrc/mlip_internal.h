@@ -1,0 +1,173 @@
+// Internal declarations of the MLIP library: context layout, constants shared
+// by host code and kernels, and the host-side launchers of each kernel file.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstddef>
+#include <cstdint>
+#include <string>
+
+#include "../../include/mlip.h"
+
+namespace mlip {
+
+// Fused-kernel geometry (gfx950: 64-wide wavefronts, 160 KB LDS per CU).
+constexpr int kWaves = 4;                 // wavefronts per work-group (one per SIMD)
+constexpr int kThreads = kWaves * 64;     // work-group size
+constexpr int kTileMax = 16;              // centre atoms per tile (k = 16, 32)
+constexpr int kEntCap = 2048;             // listed neighbour entries per tile
+constexpr int kChunkCap = kEntCap / 16 + 16;
+constexpr int kMaxSpecies = 16;
+constexpr int kEncWidth = 128;            // encoder hidden width on the GPU path
+constexpr int kHeadWidth = 64;            // head hidden width on the GPU path
+constexpr int kMaxHidden = 8;             // hidden layers supported on the GPU path
+constexpr int kAngRows = 16;              // angular rows, (lmax+1)^2 <= 16
+constexpr int kMonomials = 20;            // Cartesian monomials of degree <= 3
+
+// Number of float64 in one packed encoder table (device layout).
+inline size_t enc_table_doubles(int k, int enc_hidden) {
+  return 2 * kEncWidth + size_t(enc_hidden - 1) * (kEncWidth * kEncWidth + kEncWidth) +
+         size_t(k) * kEncWidth + k;
+}
+// Number of float64 in one packed head table (device layout).
+inline size_t head_table_doubles(int nin, int reg_hidden) {
+  return 2 * size_t(kHeadWidth) * nin + kHeadWidth +
+         size_t(reg_hidden - 1) * (2 * kHeadWidth * kHeadWidth + kHeadWidth) + kHeadWidth + 1;
+}
+
+// Arguments of the fused energy/force/virial kernel.
+struct FusedArgs {
+  const double* pos;          // caller order [n][3]
+  const int32_t* types;       // caller order [n] (library copy)
+  const int32_t* perm;        // sorted slot -> caller index
+  const int64_t* offsets;     // [n+1], rows in sorted order
+  const int32_t* idx;         // neighbour entries, caller indices
+  const double* enc;          // packed encoder tables
+  const double* head;         // packed head tables
+  const double* qc;           // [16][20] angular coefficients
+  double* energy;             // [n] or null
+  double* forces;             // [n][3], zeroed before launch
+  double* virial;             // [n][9] or null
+  double* totals;             // [10]: E, W (zeroed before launch)
+  unsigned long long* counters;  // [0] active pairs (zeroed before launch)
+  double* ws;                 // per-block workspace
+  long long ws_slot;          // doubles per block slot
+  double box[3];
+  double inv_box[3];
+  double rc, rc2;
+  long long enc_stride, head_stride;
+  int C, enc_cond, reg_cond, lmax, enc_hidden, reg_hidden;
+  int tile_atoms;             // atoms per tile (<= kTileMax)
+  int n_tiles;
+  int species_start[kMaxSpecies + 1];  // first sorted slot of each species
+  int tile_start[kMaxSpecies + 1];     // first tile of each species
+};
+
+// Arguments of the neighbour-list kernels.
+struct NbrGrid {
+  double box[3];
+  double half[3];
+  double cell_scale[3];   // nc / L
+  int nc[3];
+  int ncell;
+  int C;
+  double rl2;
+};
+
+}  // namespace mlip
+
+struct mlip_ctx {
+  mlip_hparams hp{};
+  hipStream_t stream = nullptr;
+  int device = 0;
+  int n_cu = 0;
+  std::string err;
+  size_t bytes = 0;
+
+  // weights and tables
+  double* d_enc = nullptr;
+  size_t enc_stride = 0;
+  int n_enc = 0;
+  double* d_head = nullptr;
+  size_t head_stride = 0;
+  int n_head = 0;
+  double* d_qc = nullptr;
+  double* d_inv_mass = nullptr;   // per species, acceleration factor / mass
+  bool masses_set = false;
+
+  // atoms and neighbour list
+  int64_t n = 0;
+  double box[3] = {0, 0, 0};
+  bool built = false;
+  int64_t cap_atoms = 0;
+  int32_t* d_types = nullptr;
+  int32_t* d_perm = nullptr;
+  int32_t* d_key = nullptr;
+  double* d_spos = nullptr;
+  int32_t* d_rowcnt = nullptr;
+  int64_t* d_offsets = nullptr;
+  int32_t* d_idx = nullptr;
+  size_t cap_idx = 0;
+  int32_t* d_cell_count = nullptr;
+  int32_t* d_cell_start = nullptr;
+  size_t cap_keys = 0;
+  int64_t* d_scan_tmp = nullptr;
+  size_t cap_scan = 0;
+  mlip::NbrGrid grid{};
+  int species_start[mlip::kMaxSpecies + 1] = {0};
+  int64_t n_listed = 0;
+  int max_row = 0;
+  int64_t n_builds = 0;
+
+  // fused kernel
+  double* d_ws = nullptr;
+  size_t cap_ws = 0;
+  double* d_totals = nullptr;               // [16]
+  unsigned long long* d_counters = nullptr; // [4]
+  int32_t* d_flags = nullptr;               // [4]
+  double* d_reduce = nullptr;               // [4] scratch for md reductions
+  int tile_atoms = 0;
+  int64_t n_tiles = 0;
+  int n_blocks = 0;
+};
+
+namespace mlip {
+
+// angular_tables.cpp: coefficients of the irreducible angular features as
+// rows over the 20 Cartesian monomials of degree <= 3.
+bool build_angular_table(int lmax, double out[kAngRows * kMonomials], std::string* err);
+
+// neighbors.hip
+hipError_t launch_bin(const double* pos, const int32_t* types, int64_t n, const NbrGrid& g,
+                      int32_t* key, int32_t* cell_count, int32_t* flags, hipStream_t s);
+hipError_t launch_scatter(const int32_t* key, int64_t n, const int32_t* cell_start, int32_t* fill,
+                          int32_t* perm, hipStream_t s);
+hipError_t launch_sort_segments(const int32_t* cell_start, int64_t nkeys, int32_t* perm, hipStream_t s);
+hipError_t launch_gather_sorted(const double* pos, const int32_t* perm, int64_t n, const NbrGrid& g,
+                                double* spos, hipStream_t s);
+hipError_t launch_rows(const double* spos, const int32_t* perm, int64_t n, const NbrGrid& g,
+                       const int32_t* cell_start, int32_t* rowcnt, const int64_t* offsets, int32_t* idx,
+                       int32_t* flags, bool fill, hipStream_t s);
+hipError_t launch_exclusive_scan_i32_to_i32(const int32_t* in, int64_t n, int32_t* out, int64_t* tmp,
+                                            hipStream_t s);
+hipError_t launch_exclusive_scan_i32_to_i64(const int32_t* in, int64_t n, int64_t* out, int64_t* tmp,
+                                            hipStream_t s);
+size_t scan_tmp_elems(int64_t n);
+hipError_t launch_fill_i32(int32_t* p, int64_t n, int32_t v, hipStream_t s);
+hipError_t launch_fill_f64(double* p, int64_t n, double v, hipStream_t s);
+hipError_t launch_fill_u64(unsigned long long* p, int64_t n, hipStream_t s);
+
+// fused.hip
+hipError_t launch_fused(int k, const FusedArgs& a, int n_blocks, hipStream_t s);
+
+// md.hip
+hipError_t launch_md_first_half(double* pos, double* vel, const double* forces, const int32_t* types,
+                                const double* inv_mass, int64_t n, double dt, const double* ref,
+                                double* max_disp2, hipStream_t s);
+hipError_t launch_md_second_half(double* vel, const double* forces, const int32_t* types,
+                                 const double* inv_mass, int64_t n, double dt, hipStream_t s);
+hipError_t launch_md_kinetic(const double* vel, const int32_t* types, const double* inv_mass, int64_t n,
+                             double* out, hipStream_t s);
+
+}  // namespace mlip

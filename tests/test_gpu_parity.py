@@ -1,0 +1,204 @@
+"""GPU parity: the HIP path through the C ABI against the oracle on identical
+seeded inputs.  Neighbour sets must be identical; E_i, F_i and the per-atom
+virial must agree to max-abs 1e-9 (float64 path)."""
+import numpy as np
+import pytest
+
+import synth
+import oracle
+from oracle.model import Model, evaluate
+from oracle.neighbors import brute_force_neighbors, neighbor_list
+from tests.gpu_helpers import gpu_eval, to_dev, assert_same_neighbor_sets, max_abs, log
+
+pytestmark = pytest.mark.gpu
+
+TOL = 1e-9          # eV and eV/A, float64 path
+TOL_VIRIAL = 1e-9   # eV
+
+
+def _compare(w_hp, weights, pos, types, box, label):
+    log(f"[parity] {label}: N={len(pos)}")
+    g = gpu_eval(w_hp, weights, pos, types, box)
+    m = Model(w_hp, weights)
+    off, idx = neighbor_list(pos, box, m.rc + m.skin)
+    goff, gidx = g["pot"].neighbors()
+    assert_same_neighbor_sets(goff, gidx, off, idx)
+    ref = evaluate(m, pos, types, box, off, idx)
+    eE = max_abs(g["E_i"], ref["E_i"])
+    eF = max_abs(g["F"], ref["F"])
+    eV = max_abs(g["virial"], ref["virial"])
+    log(f"[parity] {label}: max|dE|={eE:.3e} max|dF|={eF:.3e} max|dW|={eV:.3e} "
+        f"|E|max={np.abs(ref['E_i']).max():.1f} |F|max={np.abs(ref['F']).max():.1f}")
+    assert eE <= TOL, eE
+    assert eF <= TOL, eF
+    assert eV <= TOL_VIRIAL, eV
+    tot = g["totals"]
+    assert abs(tot[0] - ref["E"]) <= TOL * len(pos)
+    assert max_abs(tot[1:], ref["W"]) <= TOL_VIRIAL * len(pos)
+    st = g["stats"]
+    i_act = oracle.neighbors.active_rows(pos, box, off, idx, m.rc)[0]
+    assert st["n_active_pairs"] == len(i_act)
+    assert st["n_listed_pairs"] == len(idx)
+    g["pot"].close()
+    return g, ref
+
+
+VARIANTS = {
+    "default": {},
+    "lmax0": {"lmax": 0},
+    "lmax1": {"lmax": 1},
+    "lmax2": {"lmax": 2},
+    "enc_universal": {"enc_cond": 0},
+    "enc_neighbour": {"enc_cond": 1},
+    "head_universal": {"reg_cond": 0},
+    "enc_hidden1": {"enc_hidden": 1},
+    "enc_hidden2_reg2": {"enc_hidden": 2, "reg_hidden": 2},
+    "deep": {"enc_hidden": 5, "reg_hidden": 6},
+}
+
+
+@pytest.mark.parametrize("variant", list(VARIANTS))
+def test_binary_fcc_variants(variant):
+    w = synth.make_workload("fcc-binary-4", seed=3, hp_overrides=VARIANTS[variant])
+    _compare(w.hp, w.weights, w.pos, w.types, w.box, f"fcc-binary-4/{variant}")
+
+
+@pytest.mark.parametrize("name,n", [("fcc-ternary-64", 4), ("fcc-hea6-128", 5), ("bcc-unary-32", 6),
+                                    ("bcc-hea6-sweep", 5)])
+def test_preset_shapes(name, n):
+    w = synth.make_workload(name, seed=5, n=n)
+    _compare(w.hp, w.weights, w.pos, w.types, w.box, f"{name}/n={n}")
+
+
+def test_ragged_random_species_and_order():
+    """Species counts that do not fill tiles, shuffled atom order, positions
+    outside [0, L)."""
+    rng = np.random.default_rng(17)
+    w = synth.make_workload("fcc-hea6-128", seed=9, n=4)
+    perm = rng.permutation(len(w.pos))
+    pos = w.pos[perm] + w.box * rng.integers(-2, 3, (len(w.pos), 3))
+    types = w.types[perm].copy()
+    types[:37] = 5
+    _compare(w.hp, w.weights, pos, types, w.box, "ragged")
+
+
+def test_sparse_gas_with_isolated_atoms():
+    rng = np.random.default_rng(4)
+    box = np.array([40.0, 41.0, 43.0])
+    cl = synth.random_cluster(rng, 30, 3, 6.0, min_dist=2.0) + 20.0
+    iso = np.array([[2.0, 2.0, 2.0], [2.0, 30.0, 12.0], [35.0, 4.0, 30.0]])
+    pos = np.concatenate([cl, iso])
+    types = rng.integers(0, 3, len(pos)).astype(np.int32)
+    hp = synth.HParams(n_species=3)
+    wts = synth.random_weights(hp, 8)
+    g, ref = _compare(hp, wts, pos, types, box, "sparse")
+    assert np.all(g["F"][-3:] == 0.0)
+
+
+def test_single_atom():
+    hp = synth.HParams(n_species=2)
+    wts = synth.random_weights(hp, 2)
+    pos = np.array([[1.0, 2.0, 3.0]])
+    _compare(hp, wts, pos, np.array([1], dtype=np.int32), np.array([15.0, 15.0, 15.0]), "single")
+
+
+@pytest.mark.parametrize("shape,n,seed", [((13.0, 13.0, 13.0), 150, 1), ((14.0, 19.5, 27.0), 300, 2),
+                                          ((30.0, 30.0, 13.1), 600, 3)])
+def test_neighbor_sets_bit_exact_random(shape, n, seed):
+    """Random positions (some outside [0, L)), 1 to 4 cells per axis."""
+    torch = pytest.importorskip("torch")
+    from paper_2608_16329_amd import Potential
+    rng = np.random.default_rng(seed)
+    box = np.array(shape)
+    pos = rng.uniform(0, 1, (n, 3)) * box
+    pos[:20] += box * rng.integers(-3, 4, (20, 3))
+    types = rng.integers(0, 2, n).astype(np.int32)
+    hp = synth.HParams(n_species=2)
+    log(f"[nbr] random box {shape} N={n}")
+    pot = Potential(hp, synth.random_weights(hp, 0))
+    pot.build_neighbors(to_dev(pos), to_dev(types), box)
+    goff, gidx = pot.neighbors()
+    off, idx = brute_force_neighbors(pos, box, hp.cutoff + hp.skin)
+    assert_same_neighbor_sets(goff, gidx, off, idx)
+    pot.close()
+
+
+def test_neighbor_boundary_pairs():
+    """Pairs at exactly r_c + skin (excluded), one ulp inside (included),
+    and across the periodic face."""
+    from paper_2608_16329_amd import Potential
+    box = np.array([20.0, 20.0, 20.0])
+    below = np.nextafter(6.5, 0.0)
+    pos = np.array([[1.0, 1.0, 1.0], [7.5, 1.0, 1.0], [1.0, 1.0 + below, 1.0], [1.0, 1.0, 14.5],
+                    [10.0, 10.0, 10.0], [10.0, 16.5, 10.0], [19.999999999, 5.0, 5.0], [-1e-12, 5.0, 5.0]])
+    types = np.zeros(len(pos), dtype=np.int32)
+    hp = synth.HParams(n_species=1)
+    log("[nbr] boundary pairs")
+    pot = Potential(hp, synth.random_weights(hp, 0))
+    pot.build_neighbors(to_dev(pos), to_dev(types), box)
+    goff, gidx = pot.neighbors()
+    off, idx = brute_force_neighbors(pos, box, 6.5)
+    assert_same_neighbor_sets(goff, gidx, off, idx)
+    rows = [set(gidx[goff[i]:goff[i + 1]].tolist()) for i in range(len(pos))]
+    assert 1 not in rows[0] and 2 in rows[0] and 3 not in rows[0] and 5 not in rows[4]
+    assert 7 in rows[6]
+    pot.close()
+
+
+def test_error_paths():
+    from paper_2608_16329_amd import Potential, MlipError
+    torch = pytest.importorskip("torch")
+    hp = synth.HParams(n_species=2)
+    pot = Potential(hp, synth.random_weights(hp, 0))
+    pos = to_dev(np.zeros((4, 3)))
+    F = torch.zeros((4, 3), dtype=torch.float64, device="cuda:0")
+    with pytest.raises(MlipError, match="STATE"):
+        pot.compute(pos, F)
+    with pytest.raises(MlipError, match="BOX"):
+        pot.build_neighbors(pos, to_dev(np.zeros(4, np.int32)), [10.0, 20.0, 20.0])
+    with pytest.raises(MlipError, match="TYPE"):
+        pot.build_neighbors(to_dev(np.random.default_rng(0).uniform(0, 20, (4, 3))),
+                            to_dev(np.array([0, 1, 2, 0], np.int32)), [20.0, 20.0, 20.0])
+    bad = np.random.default_rng(0).uniform(0, 20, (4, 3))
+    bad[2, 1] = np.nan
+    with pytest.raises(MlipError, match="TYPE"):
+        pot.build_neighbors(to_dev(bad), to_dev(np.zeros(4, np.int32)), [20.0, 20.0, 20.0])
+    pot.close()
+    with pytest.raises(MlipError, match="ARG"):
+        Potential(synth.HParams(n_species=2, k=24), np.zeros(10))
+
+
+def test_md_trajectory_per_step_parity():
+    """Ten velocity-Verlet steps on the GPU; at every step the oracle is fed
+    the GPU's own positions (the list rebuilt on the same schedule)."""
+    torch = pytest.importorskip("torch")
+    from paper_2608_16329_amd import Potential
+    w = synth.make_workload("fcc-binary-4", seed=1)
+    m = Model(w.hp, w.weights)
+    pot = Potential(w.hp, w.weights)
+    pot.set_masses(w.masses)
+    pos = to_dev(w.pos)
+    vel = to_dev(w.vel)
+    types = to_dev(w.types)
+    ref = pos.clone()
+    n = len(w.pos)
+    F = torch.zeros((n, 3), dtype=torch.float64, device="cuda:0")
+    pot.build_neighbors(pos, types, w.box)
+    pot.compute(pos, F)
+    ke0 = pot.kinetic(vel)
+    v_h = w.vel.copy()
+    assert abs(ke0 - 0.5 * (w.masses[w.types][:, None] * v_h ** 2).sum() / 9.648533212e-3) < 1e-9 * ke0
+    for step in range(1, 11):
+        d2 = pot.md_first_half(pos, vel, F, 1.0, ref)
+        if step % 10 == 0 or d2 > (0.5 * w.hp.skin) ** 2:
+            pot.build_neighbors(pos, types, w.box)
+            ref.copy_(pos)
+        pot.compute(pos, F)
+        pot.md_second_half(vel, F, 1.0)
+        torch.cuda.synchronize()
+        p = pos.cpu().numpy()
+        r = evaluate(m, p, w.types, w.box)
+        err = max_abs(F.cpu().numpy(), r["F"])
+        log(f"[md] step {step}: max|dF|={err:.3e} |F|max={np.abs(r['F']).max():.1f}")
+        assert err <= TOL
+    pot.close()
