@@ -64,26 +64,24 @@ def cpu_baseline(w, target_atoms: int) -> dict:
     the centre atoms inside a cube of the supercell, with neighbours taken
     from the surrounding atoms (evaluation only, no neighbour search)."""
     import multiprocessing as mp
-    from oracle.neighbors import neighbors_of
+    from oracle.neighbors import cell_list_neighbors
 
     rl = w.hp.cutoff + w.hp.skin
     box = w.box
-    c0 = box / 2.0
-    d = w.pos - c0
+    d = w.pos - box / 2.0
     d -= box * np.round(d / box)
     rho = len(w.pos) / float(np.prod(box))
     half = 0.5 * (target_atoms / rho) ** (1.0 / 3.0)
+    reach = half + rl + 0.5
     inner = np.all(np.abs(d) < half, axis=1)
-    outer = np.all(np.abs(d) < half + rl + 0.5, axis=1)
+    outer = np.all(np.abs(d) < reach, axis=1)
     loc = np.nonzero(outer)[0]
-    lpos = d[loc] + 500.0
+    # local, non-periodic frame: a box wide enough that no periodic image is in range
+    lbox = np.full(3, 2.0 * reach + 2.0 * rl)
+    lpos = d[loc] + reach + rl
     ltypes = w.types[loc]
-    lbox = np.array([1000.0, 1000.0, 1000.0])
     centres = np.nonzero(inner[loc])[0]
-    rows = neighbors_of(lpos, lbox, rl, range(len(lpos)))
-    off = np.zeros(len(lpos) + 1, dtype=np.int64)
-    np.cumsum([len(r) for r in rows], out=off[1:])
-    idx = np.concatenate(rows).astype(np.int32)
+    off, idx = cell_list_neighbors(lpos, lbox, rl)
     cores = min(16, len(os.sched_getaffinity(0)))
     chunks = np.array_split(centres, cores)
     jobs = [(w.hp, w.weights, lpos, ltypes, lbox, off, idx, c) for c in chunks if len(c)]
@@ -107,7 +105,7 @@ def main() -> int:
     ap.add_argument("--cells", type=int, default=None, help="supercell edge override (cells)")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--rebuild-every", type=int, default=10)
-    ap.add_argument("--cpu-sample", type=int, default=3000, help="oracle sample size (atoms); 0 disables")
+    ap.add_argument("--cpu-sample", type=int, default=12000, help="oracle sample size (atoms); 0 disables")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
