@@ -105,7 +105,7 @@ def main() -> int:
     ap.add_argument("--cells", type=int, default=None, help="supercell edge override (cells)")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--rebuild-every", type=int, default=10)
-    ap.add_argument("--cpu-sample", type=int, default=12000, help="oracle sample size (atoms); 0 disables")
+    ap.add_argument("--cpu-sample", type=int, default=100000, help="oracle sample size (atoms); 0 disables")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:

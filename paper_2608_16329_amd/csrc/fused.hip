@@ -41,7 +41,46 @@ __device__ __forceinline__ v4d mfma(double a, double b, v4d c) {
   return __builtin_amdgcn_mfma_f64_16x16x4f64(a, b, c, 0, 0, 0);
 }
 
-__device__ __forceinline__ double sigmoid(double z) { return 1.0 / (1.0 + exp(-z)); }
+// Logistic sigmoid 1 / (1 + exp(-z)) in float64, written out so the VALU
+// cost stays low next to the MFMA work:
+//  * exp(t), t = -z clamped to [-700, 700] (beyond that the sigmoid is 0 or 1
+//    to far below float64 resolution of the SiLU value), by Cody-Waite
+//    reduction t = n ln2 + r with |r| <= ln2/2, the Taylor polynomial of
+//    degree 13 (truncation error below 5e-18 relative) and a 2^n scaling;
+//  * 1 / (1 + e) from the hardware reciprocal estimate refined by two
+//    Newton-Raphson steps (each squares the relative error).
+__device__ __forceinline__ double sigmoid(double z) {
+  constexpr double kLog2e = 1.4426950408889634;
+  constexpr double kLn2Hi = 6.93147180369123816490e-01;  // ln2 split, high part exact in 32 bits
+  constexpr double kLn2Lo = 1.90821492927058770002e-10;
+  const double t = fmin(fmax(-z, -700.0), 700.0);
+  const double n = rint(t * kLog2e);
+  double r = fma(-n, kLn2Hi, t);
+  r = fma(-n, kLn2Lo, r);
+  constexpr double c[14] = {
+    1.6059043836821613e-10,
+    2.08767569878681e-09,
+    2.505210838544172e-08,
+    2.755731922398589e-07,
+    2.7557319223985893e-06,
+    2.48015873015873e-05,
+    0.0001984126984126984,
+    0.001388888888888889,
+    0.008333333333333333,
+    0.041666666666666664,
+    0.16666666666666666,
+    0.5,
+    1.0,
+    1.0};
+  double p = c[0];
+#pragma unroll
+  for (int k = 1; k < 14; ++k) p = fma(p, r, c[k]);
+  const double d = 1.0 + ldexp(p, int(n));
+  double y = __builtin_amdgcn_rcp(d);
+  y = fma(fma(-d, y, 1.0), y, y);
+  y = fma(fma(-d, y, 1.0), y, y);
+  return y;
+}
 
 __device__ __forceinline__ double fold(double d, double L, double invL) { return d - L * rint(d * invL); }
 
@@ -157,30 +196,42 @@ __device__ void pass1_chunk(const FusedArgs& A, Smem<K, TM>& S, int ch, double* 
   for (int t = 1; t < A.enc_hidden; ++t) {
     const double* __restrict__ frag = layer + lane;
     const double* __restrict__ bias = layer + kEncWidth * kEncWidth;
+    // the forward accumulators start from the bias (loaded with the first
+    // fragments, so its latency overlaps theirs); the tangent has none
     v4d acc[8], dacc[8];
 #pragma unroll
     for (int To = 0; To < 8; ++To) {
-      acc[To] = v4d{0, 0, 0, 0};
+      acc[To] = v4d{bias[16 * To + g], bias[16 * To + 4 + g], bias[16 * To + 8 + g], bias[16 * To + 12 + g]};
       dacc[To] = v4d{0, 0, 0, 0};
     }
+    // weight fragments stream from L2 through a 3-deep register ring,
+    // issued two k-steps ahead of the MFMAs that consume them
+    double wb[3][8];
 #pragma unroll
-    for (int T = 0; T < 8; ++T)
+    for (int To = 0; To < 8; ++To) {
+      wb[0][To] = frag[(0 * 8 + To) * 64];
+      wb[1][To] = frag[(1 * 8 + To) * 64];
+    }
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        double w[8];
+    for (int ks = 0; ks < 32; ++ks) {
+      if (ks + 2 < 32) {
 #pragma unroll
-        for (int To = 0; To < 8; ++To) w[To] = frag[((T * 4 + i) * 8 + To) * 64];
-#pragma unroll
-        for (int To = 0; To < 8; ++To) {
-          acc[To] = mfma(w[To], h[T][i], acc[To]);
-          dacc[To] = mfma(w[To], dh[T][i], dacc[To]);
-        }
+        for (int To = 0; To < 8; ++To) wb[(ks + 2) % 3][To] = frag[((ks + 2) * 8 + To) * 64];
       }
+      __builtin_amdgcn_sched_barrier(0);
+      const int T = ks >> 2, i = ks & 3;
+#pragma unroll
+      for (int To = 0; To < 8; ++To) {
+        acc[To] = mfma(wb[ks % 3][To], h[T][i], acc[To]);
+        dacc[To] = mfma(wb[ks % 3][To], dh[T][i], dacc[To]);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    }
 #pragma unroll
     for (int To = 0; To < 8; ++To)
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
-        const double z = acc[To][q] + bias[16 * To + 4 * q + g];
+        const double z = acc[To][q];
         const double s = sigmoid(z);
         h[To][q] += z * s;
         dh[To][q] += s * (1.0 + z * (1.0 - s)) * dacc[To][q];
@@ -190,32 +241,37 @@ __device__ void pass1_chunk(const FusedArgs& A, Smem<K, TM>& S, int ch, double* 
 
   // output layer with pairs as rows: m[pair 4q+g][16Tc + c]
   v4d mo[KT], dmo[KT];
-#pragma unroll
-  for (int Tc = 0; Tc < KT; ++Tc) {
-    mo[Tc] = v4d{0, 0, 0, 0};
-    dmo[Tc] = v4d{0, 0, 0, 0};
-  }
   {
-    const double* __restrict__ frag = layer + lane;
-#pragma unroll
-    for (int T = 0; T < 8; ++T)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        double w[KT];
-#pragma unroll
-        for (int Tc = 0; Tc < KT; ++Tc) w[Tc] = frag[((T * 4 + i) * KT + Tc) * 64];
-#pragma unroll
-        for (int Tc = 0; Tc < KT; ++Tc) {
-          mo[Tc] = mfma(h[T][i], w[Tc], mo[Tc]);
-          dmo[Tc] = mfma(dh[T][i], w[Tc], dmo[Tc]);
-        }
-      }
     const double* __restrict__ bout = layer + K * kEncWidth;
 #pragma unroll
     for (int Tc = 0; Tc < KT; ++Tc) {
       const double b = bout[16 * Tc + c];
+      mo[Tc] = v4d{b, b, b, b};
+      dmo[Tc] = v4d{0, 0, 0, 0};
+    }
+  }
+  {
+    const double* __restrict__ frag = layer + lane;
+    double wb[3][KT];
 #pragma unroll
-      for (int q = 0; q < 4; ++q) mo[Tc][q] += b;
+    for (int Tc = 0; Tc < KT; ++Tc) {
+      wb[0][Tc] = frag[(0 * KT + Tc) * 64];
+      wb[1][Tc] = frag[(1 * KT + Tc) * 64];
+    }
+#pragma unroll
+    for (int ks = 0; ks < 32; ++ks) {
+      if (ks + 2 < 32) {
+#pragma unroll
+        for (int Tc = 0; Tc < KT; ++Tc) wb[(ks + 2) % 3][Tc] = frag[((ks + 2) * KT + Tc) * 64];
+      }
+      __builtin_amdgcn_sched_barrier(0);
+      const int T = ks >> 2, i = ks & 3;
+#pragma unroll
+      for (int Tc = 0; Tc < KT; ++Tc) {
+        mo[Tc] = mfma(h[T][i], wb[ks % 3][Tc], mo[Tc]);
+        dmo[Tc] = mfma(dh[T][i], wb[ks % 3][Tc], dmo[Tc]);
+      }
+      __builtin_amdgcn_sched_barrier(0);
     }
   }
 
