@@ -109,17 +109,24 @@ size_t head_blob_doubles(const mlip_hparams* hp) {
   return R * nin + R + size_t(hp->reg_hidden - 1) * (R * R + R) + R + 1;
 }
 
-// Fragment order of a [out][128] matrix for MFMA 16x16x4: block (T, i, t)
-// holds, at lane 16 g + c, element [16 t + c][16 T + 4 i + g].
-void pack_fragments(const double* M, int nout, std::vector<double>* out) {
-  const int tiles = nout / 16;
-  for (int T = 0; T < 8; ++T)
+// Fragment order of a row-major [nout][nin] matrix for MFMA 16x16x4: block
+// (T, i, t) holds, at lane 16 g + c, element [16 t + c][16 T + 4 i + g], so
+// one wavefront load of a block is one contiguous 512-byte read.
+void pack_fragments(const double* M, int nout, int nin, std::vector<double>* out) {
+  for (int T = 0; T < nin / 16; ++T)
     for (int i = 0; i < 4; ++i)
-      for (int t = 0; t < tiles; ++t)
+      for (int t = 0; t < nout / 16; ++t)
         for (int lane = 0; lane < 64; ++lane) {
           const int g = lane >> 4, c = lane & 15;
-          out->push_back(M[size_t(16 * t + c) * kEncWidth + 16 * T + 4 * i + g]);
+          out->push_back(M[size_t(16 * t + c) * nin + 16 * T + 4 * i + g]);
         }
+}
+
+std::vector<double> transpose(const double* M, int rows, int cols) {
+  std::vector<double> t(size_t(rows) * cols);
+  for (int r = 0; r < rows; ++r)
+    for (int c = 0; c < cols; ++c) t[size_t(c) * rows + r] = M[size_t(r) * cols + c];
+  return t;
 }
 
 }  // namespace
@@ -167,29 +174,28 @@ mlip_status mlip_create(const mlip_hparams* hp, const double* weights_host, size
     enc.insert(enc.end(), p, p + 2 * W);
     p += 2 * W;
     for (int h = 1; h < hp->enc_hidden; ++h) {
-      pack_fragments(p, kEncWidth, &enc);
+      pack_fragments(p, kEncWidth, kEncWidth, &enc);
       enc.insert(enc.end(), p + W * W, p + W * W + W);
       p += W * W + W;
     }
-    pack_fragments(p, k, &enc);
+    pack_fragments(p, k, kEncWidth, &enc);
     enc.insert(enc.end(), p + size_t(k) * W, p + size_t(k) * W + k);
   }
-  // head tables -> [A0^T | A0 | c0 | (A_t^T A_t c_t)... | a_out c_out]
+  // head tables -> [frag(A0) | frag(A0^T) | c0 | (frag(A_t) frag(A_t^T) c_t)... | a_out c_out]
   std::vector<double> head;
   head.reserve(ctx->head_stride * ctx->n_head);
   const double* hsrc = src + size_t(ctx->n_enc) * enc_blob_doubles(hp);
-  const size_t R = kHeadWidth;
+  const int R = kHeadWidth;
   for (int t = 0; t < ctx->n_head; ++t) {
     const double* p = hsrc + size_t(t) * head_blob_doubles(hp);
-    for (int in = 0; in < nin; ++in)
-      for (size_t o = 0; o < R; ++o) head.push_back(p[o * nin + in]);
-    head.insert(head.end(), p, p + R * nin);
-    head.insert(head.end(), p + R * nin, p + R * nin + R);
-    p += R * nin + R;
+    pack_fragments(p, R, nin, &head);
+    pack_fragments(transpose(p, R, nin).data(), nin, R, &head);
+    head.insert(head.end(), p + size_t(R) * nin, p + size_t(R) * nin + R);
+    p += size_t(R) * nin + R;
     for (int h = 1; h < hp->reg_hidden; ++h) {
-      for (size_t in = 0; in < R; ++in)
-        for (size_t o = 0; o < R; ++o) head.push_back(p[o * R + in]);
-      head.insert(head.end(), p, p + R * R + R);
+      pack_fragments(p, R, R, &head);
+      pack_fragments(transpose(p, R, R).data(), R, R, &head);
+      head.insert(head.end(), p + R * R, p + R * R + R);
       p += R * R + R;
     }
     head.insert(head.end(), p, p + R + 1);

@@ -122,9 +122,9 @@ __device__ __forceinline__ void monomial_grads(double x, double y, double z, dou
 template <int K, int TM>
 struct Smem {
   double P[TM][kAngRows][K + 1];  // moment, then its adjoint W (padded rows)
-  double x[TM][4 * K];            // head input vec(G)
-  double ybuf[TM][kHeadWidth];
-  double gbuf[TM][kHeadWidth];
+  double xT[4 * K][16];           // head input vec(G), feature-major
+  double yT[kHeadWidth][16];      // head activations
+  double gT[kHeadWidth][16];      // head backward scratch
   double qc[kAngRows][kMonomials];
   double tpos[TM][3];
   double Fi[TM][3];
@@ -239,18 +239,21 @@ __device__ void pass1_chunk(const FusedArgs& A, Smem<K, TM>& S, int ch, double* 
     layer += kEncWidth * kEncWidth + kEncWidth;
   }
 
-  // output layer with pairs as rows: m[pair 4q+g][16Tc + c]
+  // output layer with pairs as rows: m[pair 4q+g][16Tc + c]; even and odd
+  // k-steps accumulate separately so 4 KT independent MFMA chains are in
+  // flight
   v4d mo[KT], dmo[KT];
   {
     const double* __restrict__ bout = layer + K * kEncWidth;
+    v4d mo2[2][KT], dmo2[2][KT];
 #pragma unroll
     for (int Tc = 0; Tc < KT; ++Tc) {
       const double b = bout[16 * Tc + c];
-      mo[Tc] = v4d{b, b, b, b};
-      dmo[Tc] = v4d{0, 0, 0, 0};
+      mo2[0][Tc] = v4d{b, b, b, b};
+      mo2[1][Tc] = v4d{0, 0, 0, 0};
+      dmo2[0][Tc] = v4d{0, 0, 0, 0};
+      dmo2[1][Tc] = v4d{0, 0, 0, 0};
     }
-  }
-  {
     const double* __restrict__ frag = layer + lane;
     double wb[3][KT];
 #pragma unroll
@@ -268,10 +271,15 @@ __device__ void pass1_chunk(const FusedArgs& A, Smem<K, TM>& S, int ch, double* 
       const int T = ks >> 2, i = ks & 3;
 #pragma unroll
       for (int Tc = 0; Tc < KT; ++Tc) {
-        mo[Tc] = mfma(h[T][i], wb[ks % 3][Tc], mo[Tc]);
-        dmo[Tc] = mfma(dh[T][i], wb[ks % 3][Tc], dmo[Tc]);
+        mo2[ks & 1][Tc] = mfma(h[T][i], wb[ks % 3][Tc], mo2[ks & 1][Tc]);
+        dmo2[ks & 1][Tc] = mfma(dh[T][i], wb[ks % 3][Tc], dmo2[ks & 1][Tc]);
       }
       __builtin_amdgcn_sched_barrier(0);
+    }
+#pragma unroll
+    for (int Tc = 0; Tc < KT; ++Tc) {
+      mo[Tc] = mo2[0][Tc] + mo2[1][Tc];
+      dmo[Tc] = dmo2[0][Tc] + dmo2[1][Tc];
     }
   }
 
@@ -435,127 +443,112 @@ __device__ void pass2_chunk(const FusedArgs& A, Smem<K, TM>& S, int ch, const do
   }
 }
 
-// Descriptor, head forward/backward and W for the tile (all threads).
+// Descriptor (Eq. 5), head forward and backward (Eq. 6) and W = dE/dP
+// (Eq. 7) for the tile on MFMA: the tile's atoms are the 16 columns of every
+// product and wavefront w owns rows 16w..16w+15 of each 64-wide layer.
+// Activations live in LDS feature-major ([feature][atom]) so that B-operand
+// reads are contiguous; pre-activations stay in registers for the backward
+// pass.
 template <int K, int TM>
 __device__ void head_stage(const FusedArgs& A, Smem<K, TM>& S) {
-  const int tid = threadIdx.x;
+  constexpr int R = kHeadWidth;
+  constexpr int HS = 2 * R * R + R;  // one hidden layer: A_t and A_t^T fragments, c_t
+  const int tid = threadIdx.x, lane = tid & 63, g = lane >> 4, c = lane & 15, w = tid >> 6;
   const int na = S.na;
   const int nin = (A.lmax + 1) * K;
-  // Eq. 5: G[0,c] = P[0,c]; G[l,c] = sum over the order-l rows of P^2
-  for (int u = tid; u < na * K; u += kThreads) {
-    const int a = u / K, c = u % K;
-    S.x[a][c] = S.P[a][0][c];
-    for (int l = 1; l <= A.lmax; ++l) {
-      double sq = 0.0;
-      for (int mm = l * l; mm < (l + 1) * (l + 1); ++mm) sq += S.P[a][mm][c] * S.P[a][mm][c];
-      S.x[a][l * K + c] = sq;
+  const int tin = nin / 16;
+  for (int u = tid; u < 16 * nin; u += kThreads) {
+    const int a = u & 15, in = u >> 4;
+    double v = 0.0;
+    if (a < na) {
+      const int l = in / K, col = in % K;
+      if (l == 0) {
+        v = S.P[a][0][col];
+      } else {
+        for (int mm = l * l; mm < (l + 1) * (l + 1); ++mm) v += S.P[a][mm][col] * S.P[a][mm][col];
+      }
     }
+    S.xT[in][a] = v;
   }
   __syncthreads();
 
   const int rho = A.reg_cond ? S.tile_species : 0;
-  const double* __restrict__ ht = A.head + (long long)rho * A.head_stride;
-  const double* __restrict__ A0T = ht;                          // [nin][64]
-  const double* __restrict__ A0 = ht + kHeadWidth * nin;        // [64][nin]
-  const double* __restrict__ c0 = A0 + kHeadWidth * nin;
-  const double* __restrict__ hid = c0 + kHeadWidth;
-  const int a = tid >> 4, o4 = tid & 15;
-  const bool act = a < na;
-  double zeta[kMaxHidden][4];
+  const double* __restrict__ A0f = A.head + (long long)rho * A.head_stride;  // A0 fragments
+  const double* __restrict__ A0Tf = A0f + R * nin;                          // A0^T fragments
+  const double* __restrict__ c0 = A0Tf + R * nin;
+  const double* __restrict__ hid = c0 + R;
+  const double* __restrict__ aout = hid + (A.reg_hidden - 1) * HS;
+  const int r0 = 16 * w + g;  // this lane's rows are r0 + 4q
 
-  // Eq. 6 forward
-  if (act) {
+  // layer 0: z0 = A0 x + c0
+  v4d z0 = v4d{c0[r0], c0[r0 + 4], c0[r0 + 8], c0[r0 + 12]};
+  for (int ks = 0; ks < nin / 4; ++ks)
+    z0 = mfma(A0f[(ks * 4 + w) * 64 + lane], S.xT[16 * (ks >> 2) + 4 * (ks & 3) + g][c], z0);
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const int o = o4 + 16 * q;
-      double z = c0[o];
-      for (int in = 0; in < nin; ++in) z += A0T[in * kHeadWidth + o] * S.x[a][in];
-      zeta[0][q] = z;
-      S.ybuf[a][o] = z * sigmoid(z);
-    }
-  }
+  for (int q = 0; q < 4; ++q) S.yT[r0 + 4 * q][c] = z0[q] * sigmoid(z0[q]);
   __syncthreads();
+
+  // residual layers: y <- y + silu(A_t y + c_t)
+  v4d zeta[kMaxHidden];
 #pragma unroll
   for (int t = 1; t < kMaxHidden; ++t) {
     if (t >= A.reg_hidden) break;
-    const double* __restrict__ AtT = hid + (t - 1) * (2 * kHeadWidth * kHeadWidth + kHeadWidth);
-    const double* __restrict__ ct = AtT + 2 * kHeadWidth * kHeadWidth;
-    double z[4] = {0, 0, 0, 0};
-    if (act) {
+    const double* __restrict__ Af = hid + (t - 1) * HS;
+    const double* __restrict__ ct = Af + 2 * R * R;
+    v4d z = v4d{ct[r0], ct[r0 + 4], ct[r0 + 8], ct[r0 + 12]};
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const int o = o4 + 16 * q;
-        double acc = ct[o];
-        for (int in = 0; in < kHeadWidth; ++in) acc += AtT[in * kHeadWidth + o] * S.ybuf[a][in];
-        z[q] = acc;
-        zeta[t][q] = acc;
-      }
-    }
+    for (int ks = 0; ks < 16; ++ks) z = mfma(Af[(ks * 4 + w) * 64 + lane], S.yT[16 * (ks >> 2) + 4 * (ks & 3) + g][c], z);
+    zeta[t] = z;
     __syncthreads();
-    if (act) {
 #pragma unroll
-      for (int q = 0; q < 4; ++q) S.ybuf[a][o4 + 16 * q] += z[q] * sigmoid(z[q]);
-    }
+    for (int q = 0; q < 4; ++q) S.yT[r0 + 4 * q][c] += z[q] * sigmoid(z[q]);
     __syncthreads();
   }
-  const double* __restrict__ aout = hid + (A.reg_hidden - 1) * (2 * kHeadWidth * kHeadWidth + kHeadWidth);
-  const double cout = aout[kHeadWidth];
-  double part = 0.0;
-  double d[4];
-  if (act) {
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      part += aout[o4 + 16 * q] * S.ybuf[a][o4 + 16 * q];
-      d[q] = aout[o4 + 16 * q];
-    }
+  if (tid < na) {
+    double e = aout[R];
+    for (int o = 0; o < R; ++o) e += aout[o] * S.yT[o][tid];
+    S.Ei[tid] = e;
   }
-#pragma unroll
-  for (int o = 1; o < 16; o <<= 1) part += __shfl_xor(part, o, 64);
-  if (act && o4 == 0) S.Ei[a] = part + cout;
 
-  // backward through the residual layers: d <- d + A_t^T (silu'(zeta_t) d)
+  // backward: d <- d + A_t^T (silu'(zeta_t) d), starting from d = a_out
+  v4d d = v4d{aout[r0], aout[r0 + 4], aout[r0 + 8], aout[r0 + 12]};
 #pragma unroll
   for (int t = kMaxHidden - 1; t >= 1; --t) {
     if (t >= A.reg_hidden) continue;
-    const double* __restrict__ At = hid + (t - 1) * (2 * kHeadWidth * kHeadWidth + kHeadWidth) +
-                                    kHeadWidth * kHeadWidth;  // [64][64] row-major [out][in]
-    if (act) {
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const double z = zeta[t][q], s = sigmoid(z);
-        S.gbuf[a][o4 + 16 * q] = s * (1.0 + z * (1.0 - s)) * d[q];
-      }
-    }
-    __syncthreads();
-    if (act) {
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const int in = o4 + 16 * q;
-        double acc = 0.0;
-        for (int o = 0; o < kHeadWidth; ++o) acc += At[o * kHeadWidth + in] * S.gbuf[a][o];
-        d[q] += acc;
-      }
-    }
-    __syncthreads();
-  }
-  if (act) {
+    const double* __restrict__ ATf = hid + (t - 1) * HS + R * R;
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
-      const double z = zeta[0][q], s = sigmoid(z);
-      S.gbuf[a][o4 + 16 * q] = s * (1.0 + z * (1.0 - s)) * d[q];
+      const double z = zeta[t][q], sg = sigmoid(z);
+      S.gT[r0 + 4 * q][c] = sg * (1.0 + z * (1.0 - sg)) * d[q];
     }
+    __syncthreads();
+    v4d acc = v4d{0, 0, 0, 0};
+#pragma unroll
+    for (int ks = 0; ks < 16; ++ks) acc = mfma(ATf[(ks * 4 + w) * 64 + lane], S.gT[16 * (ks >> 2) + 4 * (ks & 3) + g][c], acc);
+    d += acc;
+    __syncthreads();
+  }
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const double z = z0[q], sg = sigmoid(z);
+    S.gT[r0 + 4 * q][c] = sg * (1.0 + z * (1.0 - sg)) * d[q];
   }
   __syncthreads();
-  // dE/dx = A0^T (silu'(zeta0) d), then Eq. 7: W = dE/dP in place of P
-  if (act) {
-    for (int in = o4; in < nin; in += 16) {
-      double acc = 0.0;
-      for (int o = 0; o < kHeadWidth; ++o) acc += A0[o * nin + in] * S.gbuf[a][o];
-      const int l = in / K, c = in % K;
-      if (l == 0) {
-        S.P[a][0][c] = acc;
-      } else {
-        for (int mm = l * l; mm < (l + 1) * (l + 1); ++mm) S.P[a][mm][c] *= 2.0 * acc;
+  // dE/dx = A0^T g0, then W[0][col] = dE/dG[0][col], W[m][col] = 2 dE/dG[l][col] P[m][col]
+  for (int tt = w; tt < tin; tt += kWaves) {
+    v4d acc = v4d{0, 0, 0, 0};
+#pragma unroll
+    for (int ks = 0; ks < 16; ++ks) acc = mfma(A0Tf[(ks * tin + tt) * 64 + lane], S.gT[16 * (ks >> 2) + 4 * (ks & 3) + g][c], acc);
+    if (c < na) {
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int in = 16 * tt + 4 * q + g;
+        const int l = in / K, col = in % K;
+        if (l == 0) {
+          S.P[c][0][col] = acc[q];
+        } else {
+          for (int mm = l * l; mm < (l + 1) * (l + 1); ++mm) S.P[c][mm][col] *= 2.0 * acc[q];
+        }
       }
     }
   }
