@@ -26,6 +26,32 @@ sys.path.insert(0, ROOT)
 
 PEAK_FP64_TFLOPS = 78.6   # MI355X dense FP64 (vector and matrix)
 PEAK_HBM_GBS = 8000.0
+FUSED_SOURCE = os.path.join(ROOT, "paper_2608_16329_amd", "csrc", "fused.hip")
+TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "k_fused_fcc-hea6-128_traffic.md")
+
+
+def fused_source_hash() -> str:
+    import hashlib
+    with open(FUSED_SOURCE, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()
+
+
+def measured_traffic(workload: str, n_atoms: int):
+    """HBM bytes per launch of the fused kernel from the committed rocprofv3
+    FETCH_SIZE / WRITE_SIZE summary, scaled by the same counters on a plain
+    copy of known size; None when the summary is for other kernel source or
+    another workload."""
+    try:
+        with open(TRAFFIC_SUMMARY) as f:
+            for line in f:
+                if line.startswith("traffic_json:"):
+                    t = json.loads(line.split(":", 1)[1])
+                    if t["fused_source_sha256"] == fused_source_hash() and t["n_atoms"] == n_atoms \
+                            and t["workload"] == workload:
+                        return t["traffic_bytes_per_launch"]
+    except (OSError, KeyError, ValueError):
+        pass
+    return None
 
 
 def flops_per_pair(hp) -> float:
@@ -42,6 +68,62 @@ def flops_per_atom(hp) -> float:
     R = hp.reg_width
     mac_head = (hp.lmax + 1) * hp.k * R + (hp.reg_hidden - 1) * R * R + R
     return 4.0 * mac_head
+
+
+def summarize_traffic(fetch_dir: str, write_dir: str, bench_log: str, copy_bytes: int, command: str) -> None:
+    """Write the traffic summary of the fused kernel from two rocprofv3 --pmc
+    runs (FETCH_SIZE, then WRITE_SIZE, KiB per dispatch).  Each counter is
+    scaled by what it reads for the calibration copy of copy_bytes bytes in
+    the same run; the result is HBM-side (L2-to-fabric) bytes per launch."""
+    import csv
+    import glob
+
+    def read(d, counter):
+        path = glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True)[0]
+        copy_vals, fused_vals = [], []
+        for r in csv.DictReader(open(path)):
+            if r["Counter_Name"] != counter:
+                continue
+            v = float(r["Counter_Value"])
+            if "copyBuffer" in r["Kernel_Name"]:
+                copy_vals.append(v)
+            elif "k_fused" in r["Kernel_Name"]:
+                fused_vals.append(v)
+        return max(copy_vals), fused_vals
+
+    fc, ff = read(fetch_dir, "FETCH_SIZE")
+    wc, wf = read(write_dir, "WRITE_SIZE")
+    f_scale = copy_bytes / (fc * 1024.0)
+    w_scale = copy_bytes / (wc * 1024.0)
+    fetch_b = float(np.mean(ff)) * 1024.0 * f_scale
+    write_b = float(np.mean(wf)) * 1024.0 * w_scale
+    b = None
+    for line in open(bench_log):
+        if line.startswith("{"):
+            b = json.loads(line)
+    t = {"fused_source_sha256": fused_source_hash(), "workload": b["config"]["workload"],
+         "n_atoms": b["config"]["n_atoms"], "fetch_kib_per_launch": float(np.mean(ff)),
+         "write_kib_per_launch": float(np.mean(wf)), "copy_bytes": copy_bytes, "copy_fetch_kib": fc,
+         "copy_write_kib": wc, "fetch_scale": f_scale, "write_scale": w_scale,
+         "traffic_bytes_per_launch": fetch_b + write_b, "launches": len(ff)}
+    with open(TRAFFIC_SUMMARY, "w") as f:
+        f.write("# HBM-side traffic of the fused energy/force/virial kernel, 6-component FCC 128^3\n\n")
+        f.write("Two rocprofv3 counter runs of the same command (one counter per run), from the repository\n"
+                "root on the GPU host:\n\n")
+        for ctr in ("FETCH_SIZE", "WRITE_SIZE"):
+            f.write(f"    cd /tmp && export TMPDIR=/tmp && timeout -s KILL 240 rocprofv3 --pmc {ctr} --kernel-trace \\\n"
+                    f"        -d <repo>/gpurun_out/<dir> -o run --output-format csv -- {command}\n\n")
+        f.write(f"Calibration: the command first copies {copy_bytes} bytes device-to-device; that copy read "
+                f"FETCH_SIZE = {fc:.0f} KiB and WRITE_SIZE = {wc:.0f} KiB, so fetch counts are scaled by "
+                f"{f_scale:.3f} and write counts by {w_scale:.3f}.\n\n")
+        f.write(f"Fused kernel, mean over {len(ff)} launches: FETCH_SIZE {np.mean(ff):.4g} KiB, WRITE_SIZE "
+                f"{np.mean(wf):.4g} KiB; scaled traffic {fetch_b / 1e9:.1f} GB read + {write_b / 1e9:.1f} GB "
+                f"written = {(fetch_b + write_b) / 1e9:.1f} GB per launch "
+                f"({(fetch_b + write_b) / b['config']['n_atoms']:.0f} B per atom).\n\n")
+        f.write("Most of it is the per-pair (m, dm) workspace round trip (2 x 256 B per active pair at k = 32);\n"
+                "the counters see L2-to-fabric requests, which include Infinity Cache hits.\n\n")
+        f.write("traffic_json: " + json.dumps(t) + "\n")
+    print(json.dumps(t))
 
 
 def log(msg: str) -> None:
@@ -106,7 +188,16 @@ def main() -> int:
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--rebuild-every", type=int, default=10)
     ap.add_argument("--cpu-sample", type=int, default=100000, help="oracle sample size (atoms); 0 disables")
+    ap.add_argument("--calibrate-copy-bytes", type=int, default=0,
+                    help="first run one device-to-device copy of this many bytes (counter calibration)")
+    ap.add_argument("--summarize-traffic", nargs=3, metavar=("FETCH_DIR", "WRITE_DIR", "BENCH_LOG"),
+                    help="write the traffic summary from two rocprofv3 --pmc runs and exit")
     args = ap.parse_args()
+    if args.summarize_traffic:
+        summarize_traffic(*args.summarize_traffic, copy_bytes=args.calibrate_copy_bytes or 2147483648,
+                          command="python3 <repo>/bench.py --steps 1 --warmup 0 --cpu-sample 0 "
+                                  "--calibrate-copy-bytes 2147483648")
+        return 0
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path "
@@ -123,6 +214,14 @@ def main() -> int:
     log(f"[bench] workload {w.description}: N={N} generated in {time.perf_counter() - t_gen:.1f}s")
     dev = torch.device("cuda:0")
     torch.cuda.init()
+    if args.calibrate_copy_bytes > 0:
+        src = torch.ones(args.calibrate_copy_bytes // 8, dtype=torch.float64, device=dev)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+        log(f"[bench] calibration copy of {args.calibrate_copy_bytes} bytes done")
     free0, total_mem = torch.cuda.mem_get_info(dev)
     pos = torch.from_numpy(w.pos).to(dev)
     vel = torch.from_numpy(w.vel).to(dev)
@@ -213,7 +312,7 @@ def main() -> int:
                    "listed_pairs_per_atom": st["n_listed_pairs"] / N, "tile_atoms": st["tile_atoms"],
                    "blocks": st["n_blocks"], "seed": args.seed},
         "roofline": {"bound": "mfma", "achieved": achieved, "peak": PEAK_FP64_TFLOPS, "unit": "TFLOP/s",
-                     "frac": achieved / PEAK_FP64_TFLOPS, "traffic": None,
+                     "frac": achieved / PEAK_FP64_TFLOPS, "traffic": measured_traffic(w.description, N),
                      "kernel": "fused energy/force/virial (k_fused)", "kernel_ms": ms_compute,
                      "algorithmic_flop_per_launch": flop},
         "hbm_bytes_per_atom": bpa,

@@ -131,15 +131,15 @@ struct Smem {
   double Wi[TM][9];
   double Ei[TM];
   long long row_beg[TM];
-  int row_len[TM];
   int ent_base[TM + 1];
   int orig[TM];
   int cnt[kMaxSpecies][TM];
   int base[kMaxSpecies][TM];
-  int ent_j[kEntCap];
+  double l0[kMaxSpecies][2][kEncWidth];  // w0, b0 of the tile's encoder tables, by neighbour species
   int pair_j[kEntCap];
-  signed char ent_s[kEntCap];
   unsigned char pair_a[kEntCap];
+  int wsum[kWaves];
+  int a0;
   int ch_start[kChunkCap];
   unsigned char ch_count[kChunkCap];
   unsigned char ch_s[kChunkCap];
@@ -151,8 +151,30 @@ struct Smem {
 
 // Pass 1 on one chunk: encoder forward + tangent, moment accumulation and
 // the workspace write of (m, dm).
+// Position of the neighbour in column c of chunk ch (or a dummy), fetched
+// one chunk ahead so its latency overlaps the previous chunk's work.
+struct PairPos {
+  double x, y, z;
+};
+
 template <int K, int TM>
-__device__ void pass1_chunk(const FusedArgs& A, Smem<K, TM>& S, int ch, double* __restrict__ wsc) {
+__device__ __forceinline__ PairPos load_pair_pos(const FusedArgs& A, const Smem<K, TM>& S, int ch) {
+  const int c = threadIdx.x & 15;
+  PairPos p{0.0, 0.0, 0.0};
+  if (c < S.ch_count[ch]) {
+    const long long j = S.pair_j[S.ch_start[ch] + c];
+    p.x = A.pos[3 * j];
+    p.y = A.pos[3 * j + 1];
+    p.z = A.pos[3 * j + 2];
+  }
+  return p;
+}
+
+// Pass 1 on one chunk: encoder forward + tangent, moment accumulation and
+// the workspace write of (m, dm).
+template <int K, int TM>
+__device__ void pass1_chunk(const FusedArgs& A, Smem<K, TM>& S, int ch, const PairPos pp,
+                            double* __restrict__ wsc) {
   constexpr int KT = K / 16;
   const int lane = threadIdx.x & 63, g = lane >> 4, c = lane & 15;
   const int start = S.ch_start[ch], count = S.ch_count[ch];
@@ -165,12 +187,10 @@ __device__ void pass1_chunk(const FusedArgs& A, Smem<K, TM>& S, int ch, double* 
   double ux = 1.0, uy = 0.0, uz = 0.0, r = 1.0, fc = 0.0;
   int atom = -1;
   if (valid) {
-    const int e = start + c;
-    const int j = S.pair_j[e];
-    atom = S.pair_a[e];
-    const double dx = fold(A.pos[3 * (long long)j] - S.tpos[atom][0], A.box[0], A.inv_box[0]);
-    const double dy = fold(A.pos[3 * (long long)j + 1] - S.tpos[atom][1], A.box[1], A.inv_box[1]);
-    const double dz = fold(A.pos[3 * (long long)j + 2] - S.tpos[atom][2], A.box[2], A.inv_box[2]);
+    atom = S.pair_a[start + c];
+    const double dx = fold(pp.x - S.tpos[atom][0], A.box[0], A.inv_box[0]);
+    const double dy = fold(pp.y - S.tpos[atom][1], A.box[1], A.inv_box[1]);
+    const double dz = fold(pp.z - S.tpos[atom][2], A.box[2], A.inv_box[2]);
     r = sqrt(dx * dx + dy * dy + dz * dz);
     const double ir = 1.0 / r;
     ux = dx * ir; uy = dy * ir; uz = dz * ir;
@@ -184,7 +204,7 @@ __device__ void pass1_chunk(const FusedArgs& A, Smem<K, TM>& S, int ch, double* 
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int in = 16 * T + 4 * i + g;
-      const double w0 = tab[in], z = w0 * r + tab[kEncWidth + in];
+      const double w0 = S.l0[sj][0][in], z = w0 * r + S.l0[sj][1][in];
       const double s = sigmoid(z);
       h[T][i] = z * s;
       dh[T][i] = s * (1.0 + z * (1.0 - s)) * w0;
@@ -206,24 +226,24 @@ __device__ void pass1_chunk(const FusedArgs& A, Smem<K, TM>& S, int ch, double* 
     }
     // weight fragments stream from L2 through a 3-deep register ring,
     // issued two k-steps ahead of the MFMAs that consume them
-    double wb[3][8];
+    constexpr int kRing = 3;  // fragments issued kRing-1 k-steps ahead
+    double wb[kRing][8];
 #pragma unroll
-    for (int To = 0; To < 8; ++To) {
-      wb[0][To] = frag[(0 * 8 + To) * 64];
-      wb[1][To] = frag[(1 * 8 + To) * 64];
-    }
+    for (int pre = 0; pre < kRing - 1; ++pre)
+#pragma unroll
+      for (int To = 0; To < 8; ++To) wb[pre][To] = frag[(pre * 8 + To) * 64];
 #pragma unroll
     for (int ks = 0; ks < 32; ++ks) {
-      if (ks + 2 < 32) {
+      if (ks + kRing - 1 < 32) {
 #pragma unroll
-        for (int To = 0; To < 8; ++To) wb[(ks + 2) % 3][To] = frag[((ks + 2) * 8 + To) * 64];
+        for (int To = 0; To < 8; ++To) wb[(ks + kRing - 1) % kRing][To] = frag[((ks + kRing - 1) * 8 + To) * 64];
       }
       __builtin_amdgcn_sched_barrier(0);
       const int T = ks >> 2, i = ks & 3;
 #pragma unroll
       for (int To = 0; To < 8; ++To) {
-        acc[To] = mfma(wb[ks % 3][To], h[T][i], acc[To]);
-        dacc[To] = mfma(wb[ks % 3][To], dh[T][i], dacc[To]);
+        acc[To] = mfma(wb[ks % kRing][To], h[T][i], acc[To]);
+        dacc[To] = mfma(wb[ks % kRing][To], dh[T][i], dacc[To]);
       }
       __builtin_amdgcn_sched_barrier(0);
     }
@@ -325,26 +345,39 @@ __device__ void pass1_chunk(const FusedArgs& A, Smem<K, TM>& S, int ch, double* 
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       const int off = (Tc * 4 + (c >> 2)) * 64 + 16 * (c & 3) + 4 * q + g;
-      wsc[off] = mo[Tc][q];
-      wsc[K * 16 + off] = dmo[Tc][q];
+      __builtin_nontemporal_store(mo[Tc][q], &wsc[off]);
+      __builtin_nontemporal_store(dmo[Tc][q], &wsc[K * 16 + off]);
     }
+}
+
+// Inputs of pass 2 for one chunk: the workspace tiles (m, dm) in B-operand
+// order and the neighbour position; loaded one chunk ahead.
+template <int K>
+struct Pass2In {
+  double mB[K / 16][4], dmB[K / 16][4];
+  PairPos pp;
+};
+
+template <int K, int TM>
+__device__ __forceinline__ void pass2_load(const FusedArgs& A, const Smem<K, TM>& S, int ch,
+                                           const double* __restrict__ wsc, Pass2In<K>& in) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int Tc = 0; Tc < K / 16; ++Tc)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      in.mB[Tc][i] = __builtin_nontemporal_load(&wsc[(Tc * 4 + i) * 64 + lane]);
+      in.dmB[Tc][i] = __builtin_nontemporal_load(&wsc[K * 16 + (Tc * 4 + i) * 64 + lane]);
+    }
+  in.pp = load_pair_pos(A, S, ch);
 }
 
 // Pass 2 on one chunk: W contractions, partial forces and scatter.
 template <int K, int TM>
-__device__ void pass2_chunk(const FusedArgs& A, Smem<K, TM>& S, int ch, const double* __restrict__ wsc) {
+__device__ void pass2_chunk(const FusedArgs& A, Smem<K, TM>& S, int ch, const Pass2In<K>& in) {
   constexpr int KT = K / 16;
   const int lane = threadIdx.x & 63, g = lane >> 4, c = lane & 15;
   const int start = S.ch_start[ch], count = S.ch_count[ch];
-
-  double mB[KT][4], dmB[KT][4];
-#pragma unroll
-  for (int Tc = 0; Tc < KT; ++Tc)
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      mB[Tc][i] = wsc[(Tc * 4 + i) * 64 + lane];
-      dmB[Tc][i] = wsc[K * 16 + (Tc * 4 + i) * 64 + lane];
-    }
 
   const bool valid = c < count;
   int atom = -1, j = 0;
@@ -353,9 +386,9 @@ __device__ void pass2_chunk(const FusedArgs& A, Smem<K, TM>& S, int ch, const do
     const int e = start + c;
     j = S.pair_j[e];
     atom = S.pair_a[e];
-    dx = fold(A.pos[3 * (long long)j] - S.tpos[atom][0], A.box[0], A.inv_box[0]);
-    dy = fold(A.pos[3 * (long long)j + 1] - S.tpos[atom][1], A.box[1], A.inv_box[1]);
-    dz = fold(A.pos[3 * (long long)j + 2] - S.tpos[atom][2], A.box[2], A.inv_box[2]);
+    dx = fold(in.pp.x - S.tpos[atom][0], A.box[0], A.inv_box[0]);
+    dy = fold(in.pp.y - S.tpos[atom][1], A.box[1], A.inv_box[1]);
+    dz = fold(in.pp.z - S.tpos[atom][2], A.box[2], A.inv_box[2]);
     r = sqrt(dx * dx + dy * dy + dz * dz);
   }
   const double ir = 1.0 / r;
@@ -374,8 +407,8 @@ __device__ void pass2_chunk(const FusedArgs& A, Smem<K, TM>& S, int ch, const do
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const double w = S.P[a][c][16 * Tc + 4 * i + g];
-        t1 = mfma(w, mB[Tc][i], t1);
-        t2 = mfma(w, dmB[Tc][i], t2);
+        t1 = mfma(w, in.mB[Tc][i], t1);
+        t2 = mfma(w, in.dmB[Tc][i], t2);
       }
     if (atom == a) {
       wm = t1;
@@ -576,18 +609,33 @@ __global__ __launch_bounds__(kThreads, 1) void k_fused(FusedArgs A) {
 
   for (int tile = lo + slot; tile < hi; tile += per) {
     // ---- A: stage atoms and rows -----------------------------------------
+    // The rows of consecutive sorted atoms are one contiguous run of the
+    // neighbour list, and each row is grouped by neighbour species, so the
+    // bucket position of an entry follows from a block-wide prefix count of
+    // active entries; every thread handles 8 consecutive entries.
     if (tid == 0) {
       int s = 0;
       while (s + 1 < A.C && tile >= A.tile_start[s + 1]) ++s;
-      const int a0 = A.species_start[s] + (tile - A.tile_start[s]) * A.tile_atoms;
-      const int rem = A.species_start[s + 1] - a0;
+      const int first = A.species_start[s] + (tile - A.tile_start[s]) * A.tile_atoms;
+      const int rem = A.species_start[s + 1] - first;
       S.tile_species = s;
       S.na = rem < A.tile_atoms ? rem : A.tile_atoms;
-      S.ent_base[0] = a0;  // temporarily the first sorted slot
+      S.a0 = first;
     }
     __syncthreads();
     const int na = S.na;
-    const int a0 = S.ent_base[0];
+    const int a0 = S.a0;
+    for (int u = tid; u < A.C * 2 * kEncWidth; u += kThreads) {
+      const int sj = u / (2 * kEncWidth), rem = u % (2 * kEncWidth);
+      const int si = S.tile_species;
+      const int tau = A.enc_cond == 2 ? si * A.C + sj : (A.enc_cond == 1 ? sj : 0);
+      S.l0[sj][rem / kEncWidth][rem % kEncWidth] = A.enc[(long long)tau * A.enc_stride + rem];
+    }
+    if (tid <= TM) {
+      const int k = tid < na ? tid : na;
+      S.ent_base[tid] = int(A.offsets[a0 + k] - A.offsets[a0]);
+      if (tid == 0) S.row_beg[0] = A.offsets[a0];
+    }
     if (tid < TM) {
       if (tid < na) {
         const int o = A.perm[a0 + tid];
@@ -595,11 +643,6 @@ __global__ __launch_bounds__(kThreads, 1) void k_fused(FusedArgs A) {
         S.tpos[tid][0] = A.pos[3 * (long long)o];
         S.tpos[tid][1] = A.pos[3 * (long long)o + 1];
         S.tpos[tid][2] = A.pos[3 * (long long)o + 2];
-        const long long b = A.offsets[a0 + tid];
-        S.row_beg[tid] = b;
-        S.row_len[tid] = int(A.offsets[a0 + tid + 1] - b);
-      } else {
-        S.row_len[tid] = 0;
       }
 #pragma unroll
       for (int k = 0; k < 3; ++k) S.Fi[tid][k] = 0.0;
@@ -610,31 +653,54 @@ __global__ __launch_bounds__(kThreads, 1) void k_fused(FusedArgs A) {
     for (int u = tid; u < kMaxSpecies * TM; u += kThreads) S.cnt[u / TM][u % TM] = 0;
     for (int u = tid; u < TM * kAngRows * (K + 1); u += kThreads) (&S.P[0][0][0])[u] = 0.0;
     __syncthreads();
-    if (tid == 0) {
-      int e = 0;
-      for (int a = 0; a < TM; ++a) {
-        S.ent_base[a] = e;
-        e += S.row_len[a];
-      }
-      S.ent_base[TM] = e;
-    }
-    __syncthreads();
-    const int nent = S.ent_base[TM];
-    for (int e = tid; e < nent; e += kThreads) {
+    const int nent = S.ent_base[na];
+    const long long ebase = S.row_beg[0];
+    constexpr int kPer = kEntCap / kThreads;
+    int ej[kPer], ea[kPer], es[kPer];
+    int my_active = 0;
+    {
+      const int e0 = tid * kPer;
       int a = 0;
-      while (a + 1 < na && e >= S.ent_base[a + 1]) ++a;
-      const int j = A.idx[S.row_beg[a] + (e - S.ent_base[a])];
-      const double dx = fold(A.pos[3 * (long long)j] - S.tpos[a][0], A.box[0], A.inv_box[0]);
-      const double dy = fold(A.pos[3 * (long long)j + 1] - S.tpos[a][1], A.box[1], A.inv_box[1]);
-      const double dz = fold(A.pos[3 * (long long)j + 2] - S.tpos[a][2], A.box[2], A.inv_box[2]);
-      const bool active = dx * dx + dy * dy + dz * dz < A.rc2;
-      const int s = A.types[j];
-      S.ent_j[e] = j;
-      S.ent_s[e] = active ? (signed char)s : (signed char)-1;
-      if (active) atomicAdd(&S.cnt[s][a], 1);
+      while (a + 1 < na && e0 >= S.ent_base[a + 1]) ++a;
+#pragma unroll
+      for (int k = 0; k < kPer; ++k) ej[k] = e0 + k < nent ? A.idx[ebase + e0 + k] : -1;
+#pragma unroll
+      for (int k = 0; k < kPer; ++k) {
+        const int e = e0 + k;
+        while (a + 1 < na && e >= S.ent_base[a + 1]) ++a;
+        ea[k] = a;
+        es[k] = -1;
+        const int j = ej[k];
+        if (j >= 0) {
+          const double dx = fold(A.pos[3 * (long long)j] - S.tpos[a][0], A.box[0], A.inv_box[0]);
+          const double dy = fold(A.pos[3 * (long long)j + 1] - S.tpos[a][1], A.box[1], A.inv_box[1]);
+          const double dz = fold(A.pos[3 * (long long)j + 2] - S.tpos[a][2], A.box[2], A.inv_box[2]);
+          if (dx * dx + dy * dy + dz * dz < A.rc2) {
+            es[k] = A.types[j];
+            atomicAdd(&S.cnt[es[k]][a], 1);
+            ++my_active;
+          }
+        }
+      }
     }
-    __syncthreads();
+    // exclusive prefix of active entries over the block (entry order)
+    int prefix;
+    {
+      int inc = my_active;
+      const int ln = tid & 63;
+#pragma unroll
+      for (int o = 1; o < 64; o <<= 1) {
+        const int t = __shfl_up(inc, o, 64);
+        if (ln >= o) inc += t;
+      }
+      if (ln == 63) S.wsum[wave] = inc;
+      __syncthreads();
+      prefix = inc - my_active;
+      for (int w = 0; w < wave; ++w) prefix += S.wsum[w];
+    }
     if (tid == 0) {
+      // bucket layout: species-major, atoms in order; chunk table; and the
+      // offset turning an entry's block-wide active prefix into its slot
       int run = 0, nch = 0;
       for (int s = 0; s < A.C; ++s) {
         const int b0 = run;
@@ -651,33 +717,58 @@ __global__ __launch_bounds__(kThreads, 1) void k_fused(FusedArgs A) {
       }
       S.n_chunks = nch;
       S.n_active = run;
+      int row_start = 0;
+      for (int a = 0; a < na; ++a) {
+        int cum = 0;
+        for (int s = 0; s < A.C; ++s) {
+          S.base[s][a] -= row_start + cum;
+          cum += S.cnt[s][a];
+        }
+        row_start += cum;
+      }
     }
     __syncthreads();
-    if (tid < na) {
-      int next[kMaxSpecies];
-      for (int s = 0; s < A.C; ++s) next[s] = S.base[s][tid];
-      const int e1 = S.ent_base[tid + 1];
-      for (int e = S.ent_base[tid]; e < e1; ++e) {
-        const int s = S.ent_s[e];
-        if (s >= 0) {
-          const int p = next[s]++;
-          S.pair_j[p] = S.ent_j[e];
-          S.pair_a[p] = (unsigned char)tid;
+#pragma unroll
+    for (int k = 0; k < kPer; ++k) {
+      if (es[k] >= 0) {
+        const int s = es[k], a = ea[k];
+        const int p = S.base[s][a] + prefix;
+        // the list builder groups every row by species, so p always lies in
+        // the (species, atom) run; the bound only keeps LDS accesses in range
+        if (p >= 0 && p < S.n_active) {
+          S.pair_j[p] = ej[k];
+          S.pair_a[p] = (unsigned char)a;
         }
+        ++prefix;
       }
     }
     __syncthreads();
 
     // ---- B: pass 1 ---------------------------------------------------------
     const int nch = S.n_chunks;
-    for (int ch = wave; ch < nch; ch += kWaves) pass1_chunk<K, TM>(A, S, ch, ws_slot + ch * chunk_doubles);
+    {
+      PairPos next = wave < nch ? load_pair_pos(A, S, wave) : PairPos{0.0, 0.0, 0.0};
+      for (int ch = wave; ch < nch; ch += kWaves) {
+        const PairPos cur = next;
+        if (ch + kWaves < nch) next = load_pair_pos(A, S, ch + kWaves);
+        pass1_chunk<K, TM>(A, S, ch, cur, ws_slot + ch * chunk_doubles);
+      }
+    }
     __syncthreads();
 
     // ---- C: descriptor, head, W ------------------------------------------
     head_stage<K, TM>(A, S);
 
     // ---- D: pass 2 ---------------------------------------------------------
-    for (int ch = wave; ch < nch; ch += kWaves) pass2_chunk<K, TM>(A, S, ch, ws_slot + ch * chunk_doubles);
+    {
+      Pass2In<K> next;
+      if (wave < nch) pass2_load(A, S, wave, ws_slot + wave * chunk_doubles, next);
+      for (int ch = wave; ch < nch; ch += kWaves) {
+        const Pass2In<K> cur = next;
+        if (ch + kWaves < nch) pass2_load(A, S, ch + kWaves, ws_slot + (ch + kWaves) * chunk_doubles, next);
+        pass2_chunk<K, TM>(A, S, ch, cur);
+      }
+    }
     __syncthreads();
 
     // ---- E: outputs --------------------------------------------------------

@@ -61,3 +61,33 @@ def assert_same_neighbor_sets(off_a, idx_a, off_b, idx_b):
 
 def max_abs(a, b):
     return float(np.max(np.abs(np.asarray(a) - np.asarray(b)))) if np.size(a) else 0.0
+
+
+def local_cluster(pos, types, box, atom, radius):
+    """Atoms within `radius` of `atom` (minimum image), re-centred in a box
+    wide enough that no periodic image is in range.  Returns the local
+    positions, species, box and the local index of `atom`."""
+    d = pos - pos[atom]
+    d -= box * np.round(d / box)
+    sel = np.nonzero((d * d).sum(1) < radius * radius)[0]
+    lbox = np.full(3, 4.0 * radius + 10.0)
+    lpos = d[sel] + lbox / 2.0
+    return lpos, types[sel], lbox, int(np.nonzero(sel == atom)[0][0]), sel
+
+
+def oracle_sample(model, pos, types, box, atoms):
+    """Oracle E_i, F_i and virial of selected atoms of a large periodic
+    system, each from a local cluster holding every centre that contributes."""
+    from oracle.model import forces_for
+    from oracle.neighbors import neighbor_list
+    rl = model.rc + model.skin
+    assert np.min(box) > 2.0 * (2.0 * rl + 1.0), "box too small for a local cluster"
+    E, F, V = [], [], []
+    for a in atoms:
+        lpos, ltypes, lbox, la, _ = local_cluster(pos, types, box, a, 2.0 * rl + 1.0)
+        off, idx = neighbor_list(lpos, lbox, rl)
+        r = forces_for(model, lpos, ltypes, lbox, [la], off, idx)
+        E.append(r["E_i"][0])
+        F.append(r["F"][0])
+        V.append(r["virial"][0])
+    return np.array(E), np.array(F), np.array(V)
