@@ -126,6 +126,105 @@ def summarize_traffic(fetch_dir: str, write_dir: str, bench_log: str, copy_bytes
     print(json.dumps(t))
 
 
+def capacity_sweep(edges, steps: int, seed: int, bpa: float = 450.0) -> None:
+    """6-component equiatomic random BCC alloy (a = 3.2 A, sigma = 0.1 A,
+    cutoff 6 A) at growing supercell edges L; "max" picks the largest L the
+    free device memory holds at the bytes per atom measured at the previous
+    edge.  Energies and virials are reduced to totals only; the skin guard
+    measures displacement against the library's build-time positions.  One
+    JSON line per edge."""
+    import torch
+    import synth
+    from paper_2608_16329_amd import Potential
+    p = synth.PRESETS["bcc-hea6-sweep"]
+    dev = torch.device("cuda:0")
+    torch.cuda.init()
+    for e in edges:
+        torch.cuda.empty_cache()
+        free0, total = torch.cuda.mem_get_info(dev)
+        if e == "max":
+            L = int(((0.93 * free0 / bpa) / 2.0) ** (1.0 / 3.0))
+        else:
+            L = int(e)
+        N = 2 * L ** 3
+        if N * bpa > 0.985 * free0:
+            print(json.dumps({"sweep_edge": L, "n_atoms": N, "fits": False}), flush=True)
+            continue
+        hp = synth.HParams(n_species=p["C"], cutoff=p["cutoff"], skin=0.5)
+        weights = synth.random_weights(hp, seed + 1)
+        masses = np.array([synth.MASS[x] for x in p["masses"]])
+        box = np.array([L * p["a"]] * 3)
+        t0 = time.perf_counter()
+        pos = torch.empty((N, 3), dtype=torch.float64, device=dev)
+        vel = torch.empty((N, 3), dtype=torch.float64, device=dev)
+        types = torch.empty(N, dtype=torch.int32, device=dev)
+        F = torch.zeros((N, 3), dtype=torch.float64, device=dev)
+        for first, cp, ct, cv in synth.lattice_stream("bcc", L, p["a"], p["C"], p["sigma"], masses, p["T"], seed):
+            m = len(cp)
+            if (first // m) % 8 == 0:
+                log(f"[sweep] L={L}: generating, {first}/{N} sites")
+            pos[first:first + m] = torch.from_numpy(cp).to(dev)
+            vel[first:first + m] = torch.from_numpy(cv).to(dev)
+            types[first:first + m] = torch.from_numpy(ct).to(dev)
+        torch.cuda.synchronize()
+        log(f"[sweep] L={L} N={N}: generated in {time.perf_counter() - t0:.1f}s")
+        pot = Potential(hp, weights)
+        pot.set_masses(masses)
+        tb = time.perf_counter()
+        pot.build_neighbors(pos, types, box)
+        torch.cuda.synchronize()
+        t_build = time.perf_counter() - tb
+        pot.compute(pos, F)
+        torch.cuda.synchronize()
+        free1, _ = torch.cuda.mem_get_info(dev)
+        used = free0 - free1
+        bpa = used / N
+        log(f"[sweep] L={L}: build {t_build:.2f}s, {bpa:.0f} B/atom")
+        rebuilds = 0
+        step = 0
+        kern = []
+        stream = torch.cuda.current_stream()
+
+        def md_step(record):
+            nonlocal step, rebuilds
+            step += 1
+            d2 = pot.md_first_half(pos, vel, F, 1.0, track=True)
+            if step % 10 == 0 or d2 > 0.0625:
+                pot.build_neighbors(pos, types, box)
+                rebuilds += 1
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            pot.compute(pos, F)
+            e1.record(stream)
+            if record:
+                kern.append((e0, e1))
+            pot.md_second_half(vel, F, 1.0)
+
+        if N < 200_000_000:   # at the largest sizes one step takes minutes: no warm-up step
+            md_step(False)
+            torch.cuda.synchronize()
+            log(f"[sweep] L={L}: warm-up step done")
+        rebuilds = 0
+        t0 = time.perf_counter()
+        for k in range(steps):
+            md_step(True)
+            torch.cuda.synchronize()
+            log(f"[sweep] L={L}: step {k + 1}/{steps} {time.perf_counter() - t0:.1f}s")
+        wall = time.perf_counter() - t0
+        st = pot.stats()
+        print(json.dumps({"sweep_edge": L, "n_atoms": N, "fits": True, "steps": steps,
+                          "atom_steps_per_s": N * steps / wall, "ms_per_step": wall / steps * 1e3,
+                          "fused_kernel_ms": float(np.mean([a.elapsed_time(b) for a, b in kern])),
+                          "hbm_bytes_per_atom": bpa, "library_bytes_per_atom": pot.memory_bytes() / N,
+                          "device_total_bytes": total, "rebuilds_in_timed_steps": rebuilds,
+                          "build_s": t_build, "listed_pairs_per_atom": st["n_listed_pairs"] / N,
+                          "active_pairs_per_atom": st["n_active_pairs"] / N,
+                          "max_atoms_estimate": int(0.97 * total / bpa)}), flush=True)
+        pot.close()
+        del pos, vel, types, F
+
+
 def log(msg: str) -> None:
     print(msg, file=sys.stderr, flush=True)
 
@@ -190,9 +289,17 @@ def main() -> int:
     ap.add_argument("--cpu-sample", type=int, default=100000, help="oracle sample size (atoms); 0 disables")
     ap.add_argument("--calibrate-copy-bytes", type=int, default=0,
                     help="first run one device-to-device copy of this many bytes (counter calibration)")
+    ap.add_argument("--sweep", default=None,
+                    help="capacity sweep over comma-separated BCC supercell edges (or 'max') and exit")
+    ap.add_argument("--sweep-steps", type=int, default=20)
+    ap.add_argument("--sweep-bpa", type=float, default=450.0,
+                    help="device bytes per atom assumed before the first edge is measured")
     ap.add_argument("--summarize-traffic", nargs=3, metavar=("FETCH_DIR", "WRITE_DIR", "BENCH_LOG"),
                     help="write the traffic summary from two rocprofv3 --pmc runs and exit")
     args = ap.parse_args()
+    if args.sweep:
+        capacity_sweep(args.sweep.split(","), args.sweep_steps, args.seed, args.sweep_bpa)
+        return 0
     if args.summarize_traffic:
         summarize_traffic(*args.summarize_traffic, copy_bytes=args.calibrate_copy_bytes or 2147483648,
                           command="python3 <repo>/bench.py --steps 1 --warmup 0 --cpu-sample 0 "

@@ -63,7 +63,7 @@ typedef struct {
   int32_t n_species;   /* C >= 1 (the GPU path supports C <= 16)                  */
   double  cutoff;      /* r_c in A                                               */
   double  skin;        /* Verlet skin in A; neighbour lists use r_c + skin       */
-  int32_t k;           /* radial feature width (GPU path: 16, 32 or 64)          */
+  int32_t k;           /* radial feature width (GPU path: 32)                    */
   int32_t lmax;        /* maximum angular order (GPU path: 0..3)                 */
   int32_t angular;     /* 0 irreducible harmonic basis, d = (lmax+1)^2
                           (1 = Cartesian monomials; not on the GPU path)         */
@@ -185,9 +185,11 @@ void mlip_destroy(mlip_ctx* ctx);
 mlip_status mlip_md_set_masses(mlip_ctx* ctx, const double* masses_host);
 
 /*
- * First half of a step: vel += dt/2 * a(F); pos += dt * vel.  If ref_dev is
- * non-NULL (float64 [n][3]) and max_disp2_host is non-NULL, the largest
- * squared displacement |pos - ref|^2 is written there (synchronises).
+ * First half of a step: vel += dt/2 * a(F); pos += dt * vel.  If
+ * max_disp2_host is non-NULL the largest squared displacement is written
+ * there (synchronises): against ref_dev (float64 [n][3]) when it is non-NULL,
+ * otherwise against the positions of the last neighbour build (minimum image,
+ * no extra memory).
  */
 mlip_status mlip_md_first_half(mlip_ctx* ctx, double* pos_dev, double* vel_dev,
                                const double* forces_dev, double dt, const double* ref_dev,

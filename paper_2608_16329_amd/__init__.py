@@ -66,9 +66,11 @@ class Potential:
     def set_masses(self, masses) -> None:
         binding.mlip_md_set_masses(self.ctx, masses)
 
-    def md_first_half(self, pos, vel, forces, dt, ref=None) -> Optional[float]:
+    def md_first_half(self, pos, vel, forces, dt, ref=None, track: bool = False) -> Optional[float]:
+        """Half kick + drift; returns the largest squared displacement since
+        `ref` (or, with track=True and no ref, since the last neighbour build)."""
         return binding.mlip_md_first_half(self.ctx, pos.data_ptr(), vel.data_ptr(), forces.data_ptr(), dt,
-                                          ref.data_ptr() if ref is not None else None)
+                                          ref.data_ptr() if ref is not None else None, track)
 
     def md_second_half(self, vel, forces, dt) -> None:
         binding.mlip_md_second_half(self.ctx, vel.data_ptr(), forces.data_ptr(), dt)

@@ -163,8 +163,8 @@ def mlip_md_set_masses(ctx: int, masses) -> None:
 
 
 def mlip_md_first_half(ctx: int, pos_ptr: int, vel_ptr: int, forces_ptr: int, dt: float,
-                       ref_ptr: Optional[int] = None) -> Optional[float]:
-    out = np.zeros(1) if ref_ptr else None
+                       ref_ptr: Optional[int] = None, track: bool = False) -> Optional[float]:
+    out = np.zeros(1) if (ref_ptr or track) else None
     _check(ctx, _lib.mlip_md_first_half(ctx, pos_ptr, vel_ptr, forces_ptr, float(dt), ref_ptr or None, _dp(out)))
     return float(out[0]) if out is not None else None
 

@@ -485,10 +485,13 @@ mlip_status mlip_md_first_half(mlip_ctx* ctx, double* pos_dev, double* vel_dev, 
   if (!ctx) return MLIP_E_ARG;
   if (!pos_dev || !vel_dev || !forces_dev) return fail(ctx, MLIP_E_ARG, "NULL argument");
   if (!ctx->built || !ctx->masses_set) return fail(ctx, MLIP_E_STATE, "build neighbours and set masses first");
-  const bool track = ref_dev && max_disp2_host;
+  const bool track = max_disp2_host != nullptr;
   if (track) MLIP_HIP(ctx, launch_fill_f64(ctx->d_reduce, 1, 0.0, ctx->stream));
   MLIP_HIP(ctx, launch_md_first_half(pos_dev, vel_dev, forces_dev, ctx->d_types, ctx->d_inv_mass, ctx->n, dt,
                                      track ? ref_dev : nullptr, ctx->d_reduce, ctx->stream));
+  if (track && !ref_dev)
+    MLIP_HIP(ctx, launch_md_disp_since_build(pos_dev, ctx->d_perm, ctx->d_spos, ctx->n, ctx->box, ctx->d_reduce,
+                                             ctx->stream));
   if (track) {
     MLIP_HIP(ctx, hipMemcpyAsync(max_disp2_host, ctx->d_reduce, sizeof(double), hipMemcpyDeviceToHost, ctx->stream));
     MLIP_HIP(ctx, hipStreamSynchronize(ctx->stream));

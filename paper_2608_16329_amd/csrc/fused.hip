@@ -345,8 +345,8 @@ __device__ void pass1_chunk(const FusedArgs& A, Smem<K, TM>& S, int ch, const Pa
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       const int off = (Tc * 4 + (c >> 2)) * 64 + 16 * (c & 3) + 4 * q + g;
-      __builtin_nontemporal_store(mo[Tc][q], &wsc[off]);
-      __builtin_nontemporal_store(dmo[Tc][q], &wsc[K * 16 + off]);
+      wsc[off] = mo[Tc][q];
+      wsc[K * 16 + off] = dmo[Tc][q];
     }
 }
 
@@ -366,8 +366,8 @@ __device__ __forceinline__ void pass2_load(const FusedArgs& A, const Smem<K, TM>
   for (int Tc = 0; Tc < K / 16; ++Tc)
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      in.mB[Tc][i] = __builtin_nontemporal_load(&wsc[(Tc * 4 + i) * 64 + lane]);
-      in.dmB[Tc][i] = __builtin_nontemporal_load(&wsc[K * 16 + (Tc * 4 + i) * 64 + lane]);
+      in.mB[Tc][i] = wsc[(Tc * 4 + i) * 64 + lane];
+      in.dmB[Tc][i] = wsc[K * 16 + (Tc * 4 + i) * 64 + lane];
     }
   in.pp = load_pair_pos(A, S, ch);
 }

@@ -165,6 +165,8 @@ hipError_t launch_fused(int k, const FusedArgs& a, int n_blocks, hipStream_t s);
 hipError_t launch_md_first_half(double* pos, double* vel, const double* forces, const int32_t* types,
                                 const double* inv_mass, int64_t n, double dt, const double* ref,
                                 double* max_disp2, hipStream_t s);
+hipError_t launch_md_disp_since_build(const double* pos, const int32_t* perm, const double* spos, int64_t n,
+                                     const double box[3], double* max_disp2, hipStream_t s);
 hipError_t launch_md_second_half(double* vel, const double* forces, const int32_t* types,
                                  const double* inv_mass, int64_t n, double dt, hipStream_t s);
 hipError_t launch_md_kinetic(const double* vel, const int32_t* types, const double* inv_mass, int64_t n,

@@ -224,3 +224,34 @@ def random_cluster(rng: np.random.Generator, N: int, C: int, radius: float,
         if all(np.linalg.norm(p - q) >= min_dist for q in pts):
             pts.append(p)
     return np.array(pts, dtype=np.float64)
+
+
+def lattice_stream(kind: str, n: int, a: float, C: int, sigma: float, masses, T: float, seed: int,
+                   planes: int = 16):
+    """Large cubic supercells generated a few ix-planes at a time (same site
+    order as `lattice`): yields (first_site, positions, species, velocities)
+    chunks so that no host array of the full system is needed.  Species are
+    i.i.d. uniform over C; velocities are Maxwell-Boltzmann at T per site
+    (no total-momentum removal or exact rescaling at this size)."""
+    if kind == "fcc":
+        basis = np.array([[0, 0, 0], [0, .5, .5], [.5, 0, .5], [.5, .5, 0]])
+    elif kind == "bcc":
+        basis = np.array([[0, 0, 0], [.5, .5, .5]])
+    else:
+        raise ValueError(kind)
+    rng = np.random.default_rng(seed)
+    masses = np.asarray(masses, dtype=np.float64)
+    g = np.arange(n, dtype=np.float64)
+    iy, iz = np.meshgrid(g, g, indexing="ij")
+    plane = np.stack([iy.ravel(), iz.ravel()], axis=1)
+    first = 0
+    for x0 in range(0, n, planes):
+        xs = np.arange(x0, min(n, x0 + planes), dtype=np.float64)
+        cells = np.concatenate([np.column_stack([np.full(len(plane), x), plane]) for x in xs])
+        pos = ((cells[:, None, :] + basis[None, :, :]).reshape(-1, 3) * a)
+        m = len(pos)
+        types = rng.integers(0, C, m).astype(np.int32)
+        pos += rng.normal(0.0, sigma, (m, 3))
+        vel = rng.normal(size=(m, 3)) * np.sqrt(KB_EV * T * FORCE_TO_ACC / masses[types])[:, None]
+        yield first, pos, types, vel
+        first += m
