@@ -24,10 +24,14 @@ import numpy as np
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
-PEAK_FP64_TFLOPS = 78.6   # MI355X dense FP64 (vector and matrix)
+PEAK_TFLOPS = {64: 78.6, 32: 157.3}   # MI355X dense MFMA FP64 / FP32
 PEAK_HBM_GBS = 8000.0
 FUSED_SOURCE = os.path.join(ROOT, "paper_2608_16329_amd", "csrc", "fused.hip")
-TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "k_fused_fcc-hea6-128_traffic.md")
+
+
+def traffic_summary_path(precision: int) -> str:
+    tag = "" if precision == 64 else "_f32"
+    return os.path.join(ROOT, "profiles", f"k_fused{tag}_fcc-hea6-128_traffic.md")
 
 
 def fused_source_hash() -> str:
@@ -36,18 +40,18 @@ def fused_source_hash() -> str:
         return hashlib.sha256(f.read()).hexdigest()
 
 
-def measured_traffic(workload: str, n_atoms: int):
+def measured_traffic(workload: str, n_atoms: int, precision: int):
     """HBM bytes per launch of the fused kernel from the committed rocprofv3
     FETCH_SIZE / WRITE_SIZE summary, scaled by the same counters on a plain
-    copy of known size; None when the summary is for other kernel source or
-    another workload."""
+    copy of known size; None when the summary is for other kernel source,
+    another workload or another precision."""
     try:
-        with open(TRAFFIC_SUMMARY) as f:
+        with open(traffic_summary_path(precision)) as f:
             for line in f:
                 if line.startswith("traffic_json:"):
                     t = json.loads(line.split(":", 1)[1])
                     if t["fused_source_sha256"] == fused_source_hash() and t["n_atoms"] == n_atoms \
-                            and t["workload"] == workload:
+                            and t["workload"] == workload and t.get("precision", 64) == precision:
                         return t["traffic_bytes_per_launch"]
     except (OSError, KeyError, ValueError):
         pass
@@ -101,13 +105,15 @@ def summarize_traffic(fetch_dir: str, write_dir: str, bench_log: str, copy_bytes
     for line in open(bench_log):
         if line.startswith("{"):
             b = json.loads(line)
+    precision = b["config"].get("precision", 64)
     t = {"fused_source_sha256": fused_source_hash(), "workload": b["config"]["workload"],
-         "n_atoms": b["config"]["n_atoms"], "fetch_kib_per_launch": float(np.mean(ff)),
+         "n_atoms": b["config"]["n_atoms"], "precision": precision, "fetch_kib_per_launch": float(np.mean(ff)),
          "write_kib_per_launch": float(np.mean(wf)), "copy_bytes": copy_bytes, "copy_fetch_kib": fc,
          "copy_write_kib": wc, "fetch_scale": f_scale, "write_scale": w_scale,
          "traffic_bytes_per_launch": fetch_b + write_b, "launches": len(ff)}
-    with open(TRAFFIC_SUMMARY, "w") as f:
-        f.write("# HBM-side traffic of the fused energy/force/virial kernel, 6-component FCC 128^3\n\n")
+    with open(traffic_summary_path(precision), "w") as f:
+        f.write(f"# HBM-side traffic of the fused energy/force/virial kernel (float{precision} network), "
+                "6-component FCC 128^3\n\n")
         f.write("Two rocprofv3 counter runs of the same command (one counter per run), from the repository\n"
                 "root on the GPU host:\n\n")
         for ctr in ("FETCH_SIZE", "WRITE_SIZE"):
@@ -120,13 +126,14 @@ def summarize_traffic(fetch_dir: str, write_dir: str, bench_log: str, copy_bytes
                 f"{np.mean(wf):.4g} KiB; scaled traffic {fetch_b / 1e9:.1f} GB read + {write_b / 1e9:.1f} GB "
                 f"written = {(fetch_b + write_b) / 1e9:.1f} GB per launch "
                 f"({(fetch_b + write_b) / b['config']['n_atoms']:.0f} B per atom).\n\n")
-        f.write("Most of it is the per-pair (m, dm) workspace round trip (2 x 256 B per active pair at k = 32);\n"
+        f.write(f"Most of it is the per-pair (m, dm) workspace round trip (2 x {precision * 4} B per active pair "
+                "at k = 32);\n"
                 "the counters see L2-to-fabric requests, which include Infinity Cache hits.\n\n")
         f.write("traffic_json: " + json.dumps(t) + "\n")
     print(json.dumps(t))
 
 
-def capacity_sweep(edges, steps: int, seed: int, bpa: float = 450.0) -> None:
+def capacity_sweep(edges, steps: int, seed: int, bpa: float = 450.0, precision: int = 64) -> None:
     """6-component equiatomic random BCC alloy (a = 3.2 A, sigma = 0.1 A,
     cutoff 6 A) at growing supercell edges L; "max" picks the largest L the
     free device memory holds at the bytes per atom measured at the previous
@@ -150,7 +157,7 @@ def capacity_sweep(edges, steps: int, seed: int, bpa: float = 450.0) -> None:
         if N * bpa > 0.985 * free0:
             print(json.dumps({"sweep_edge": L, "n_atoms": N, "fits": False}), flush=True)
             continue
-        hp = synth.HParams(n_species=p["C"], cutoff=p["cutoff"], skin=0.5)
+        hp = synth.HParams(n_species=p["C"], cutoff=p["cutoff"], skin=0.5, precision=precision)
         weights = synth.random_weights(hp, seed + 1)
         masses = np.array([synth.MASS[x] for x in p["masses"]])
         box = np.array([L * p["a"]] * 3)
@@ -213,7 +220,7 @@ def capacity_sweep(edges, steps: int, seed: int, bpa: float = 450.0) -> None:
             log(f"[sweep] L={L}: step {k + 1}/{steps} {time.perf_counter() - t0:.1f}s")
         wall = time.perf_counter() - t0
         st = pot.stats()
-        print(json.dumps({"sweep_edge": L, "n_atoms": N, "fits": True, "steps": steps,
+        print(json.dumps({"sweep_edge": L, "n_atoms": N, "fits": True, "steps": steps, "precision": precision,
                           "atom_steps_per_s": N * steps / wall, "ms_per_step": wall / steps * 1e3,
                           "fused_kernel_ms": float(np.mean([a.elapsed_time(b) for a, b in kern])),
                           "hbm_bytes_per_atom": bpa, "library_bytes_per_atom": pot.memory_bytes() / N,
@@ -285,6 +292,8 @@ def main() -> int:
     ap.add_argument("--workload", default="fcc-hea6-128")
     ap.add_argument("--cells", type=int, default=None, help="supercell edge override (cells)")
     ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--precision", type=int, choices=(64, 32), default=64,
+                    help="network arithmetic: 64 (float64) or 32 (float32 network, float64 geometry and sums)")
     ap.add_argument("--rebuild-every", type=int, default=10)
     ap.add_argument("--cpu-sample", type=int, default=100000, help="oracle sample size (atoms); 0 disables")
     ap.add_argument("--calibrate-copy-bytes", type=int, default=0,
@@ -298,7 +307,7 @@ def main() -> int:
                     help="write the traffic summary from two rocprofv3 --pmc runs and exit")
     args = ap.parse_args()
     if args.sweep:
-        capacity_sweep(args.sweep.split(","), args.sweep_steps, args.seed, args.sweep_bpa)
+        capacity_sweep(args.sweep.split(","), args.sweep_steps, args.seed, args.sweep_bpa, args.precision)
         return 0
     if args.summarize_traffic:
         summarize_traffic(*args.summarize_traffic, copy_bytes=args.calibrate_copy_bytes or 2147483648,
@@ -316,7 +325,8 @@ def main() -> int:
     from paper_2608_16329_amd import Potential
 
     t_gen = time.perf_counter()
-    w = synth.make_workload(args.workload, seed=args.seed, n=args.cells)
+    w = synth.make_workload(args.workload, seed=args.seed, n=args.cells,
+                            hp_overrides={"precision": args.precision})
     N = len(w.pos)
     log(f"[bench] workload {w.description}: N={N} generated in {time.perf_counter() - t_gen:.1f}s")
     dev = torch.device("cuda:0")
@@ -410,16 +420,17 @@ def main() -> int:
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "f64",
+        "dtype": "f64" if args.precision == 64 else "f32",
         "data": "synthetic",
         "config": {"workload": w.description, "n_atoms": N, "n_species": w.hp.n_species, "k": w.hp.k,
                    "lmax": w.hp.lmax, "cutoff": w.hp.cutoff, "skin": w.hp.skin, "dt_fs": dt,
                    "rebuild_every": args.rebuild_every, "rebuilds_in_timed_steps": rebuilds,
                    "active_pairs_per_atom": float(np.mean(active_pairs)) / N,
                    "listed_pairs_per_atom": st["n_listed_pairs"] / N, "tile_atoms": st["tile_atoms"],
-                   "blocks": st["n_blocks"], "seed": args.seed},
-        "roofline": {"bound": "mfma", "achieved": achieved, "peak": PEAK_FP64_TFLOPS, "unit": "TFLOP/s",
-                     "frac": achieved / PEAK_FP64_TFLOPS, "traffic": measured_traffic(w.description, N),
+                   "blocks": st["n_blocks"], "seed": args.seed, "precision": args.precision},
+        "roofline": {"bound": "mfma", "achieved": achieved, "peak": PEAK_TFLOPS[args.precision], "unit": "TFLOP/s",
+                     "frac": achieved / PEAK_TFLOPS[args.precision],
+                     "traffic": measured_traffic(w.description, N, args.precision),
                      "kernel": "fused energy/force/virial (k_fused)", "kernel_ms": ms_compute,
                      "algorithmic_flop_per_launch": flop},
         "hbm_bytes_per_atom": bpa,

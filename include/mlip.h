@@ -27,7 +27,13 @@
  *   - Every call returns a status; nothing throws or aborts across the ABI.
  *     On failure mlip_last_error(ctx) describes the cause.
  *   - A context is not thread-safe; use one context per host thread.
- *   - Float64 throughout (Section 4.1: all calculations in FP64).
+ *   - Every buffer crossing the ABI is float64 or int32.  The arithmetic of
+ *     the network is set by mlip_hparams.precision: 64 evaluates everything
+ *     in float64 (Section 4.1); 32 is the reduced-precision mode the paper
+ *     evaluates beside it (Sections 3.4 and 4.4), here with the network, the
+ *     angular features and the moment/adjoint contractions in float32 and
+ *     the pair geometry and all force, virial and energy accumulation in
+ *     float64.
  */
 #ifndef MLIP_H
 #define MLIP_H
@@ -73,7 +79,7 @@ typedef struct {
   int32_t enc_hidden;  /* encoder hidden layers (GPU path: 1..8)                 */
   int32_t reg_width;   /* head hidden width (GPU path: 64)                       */
   int32_t reg_hidden;  /* head hidden layers (GPU path: 1..8)                    */
-  int32_t precision;   /* 64                                                     */
+  int32_t precision;   /* 64 (float64) or 32 (float32 network, see above)         */
 } mlip_hparams;
 
 /* Statistics of the context (mlip_get_stats). */
@@ -111,7 +117,8 @@ size_t mlip_weight_count(const mlip_hparams* hp);
 /*
  * Create a context on the current HIP device.  Copies and repacks the
  * weights (weights_host, n_weights float64 values, layout above) into device
- * memory and builds the angular projection tables.  hip_stream is a
+ * memory, rounded to float32 when precision is 32, and builds the angular
+ * projection tables.  hip_stream is a
  * hipStream_t (NULL = default stream); all later work is enqueued on it.
  * Errors: MLIP_E_ARG (bad hparams, unsupported on the GPU path, n_weights
  * mismatch, NULL pointers), MLIP_E_OOM, MLIP_E_HIP.  On error *out is NULL.

@@ -11,10 +11,6 @@
 
 using namespace mlip;
 
-namespace mlip {
-size_t fused_smem_bytes(int k);
-}
-
 namespace {
 
 constexpr double kAccPerForceMass = 9.648533212e-3;  // (eV/A)/amu -> A/fs^2
@@ -78,7 +74,7 @@ bool structurally_valid(const mlip_hparams* hp) {
 }
 
 bool gpu_supported(const mlip_hparams* hp, std::string* why) {
-  if (hp->precision != 64) return *why = "precision must be 64", false;
+  if (hp->precision != 64 && hp->precision != 32) return *why = "precision must be 64 or 32", false;
   if (hp->angular != 0) return *why = "only the irreducible angular basis runs on the GPU path", false;
   if (hp->lmax < 0 || hp->lmax > 3) return *why = "lmax must be in 0..3 on the GPU path", false;
   if (hp->k != 32) return *why = "k must be 32 on the GPU path", false;
@@ -109,17 +105,33 @@ size_t head_blob_doubles(const mlip_hparams* hp) {
   return R * nin + R + size_t(hp->reg_hidden - 1) * (R * R + R) + R + 1;
 }
 
-// Fragment order of a row-major [nout][nin] matrix for MFMA 16x16x4: block
-// (T, i, t) holds, at lane 16 g + c, element [16 t + c][16 T + 4 i + g], so
-// one wavefront load of a block is one contiguous 512-byte read.
-void pack_fragments(const double* M, int nout, int nin, std::vector<double>* out) {
+// Fragment order of a row-major [nout][nin] matrix for MFMA 16x16x4.  The
+// fragment of block (T, i) and output tile t holds, at lane 16 g + c,
+// element [16 t + c][16 T + kin(i, g)]; kin is the row map of the MFMA
+// result registers (4 i + g for float64, 4 g + i for float32), so that a
+// result tile feeds the next product as its B operand.  Fragments of vw
+// consecutive output tiles are interleaved per lane so that one 16-byte load
+// per lane fetches vw of them: element (T, i, t, lane) sits at
+// ((((4 T + i) (nout/16/vw) + t/vw) 64 + lane) vw + t%vw.
+void pack_fragments(const double* M, int nout, int nin, int precision, int vw, std::vector<double>* out) {
+  const int nt = nout / 16;
   for (int T = 0; T < nin / 16; ++T)
     for (int i = 0; i < 4; ++i)
-      for (int t = 0; t < nout / 16; ++t)
-        for (int lane = 0; lane < 64; ++lane) {
-          const int g = lane >> 4, c = lane & 15;
-          out->push_back(M[size_t(16 * t + c) * nin + 16 * T + 4 * i + g]);
-        }
+      for (int u = 0; u < nt / vw; ++u)
+        for (int lane = 0; lane < 64; ++lane)
+          for (int v = 0; v < vw; ++v) {
+            const int g = lane >> 4, c = lane & 15, t = u * vw + v;
+            const int kin = precision == 64 ? 4 * i + g : 4 * g + i;
+            out->push_back(M[size_t(16 * t + c) * nin + 16 * T + kin]);
+          }
+}
+
+// Copy host values to the device in the kernel's arithmetic type.
+hipError_t upload(void* dev, const double* host, size_t n, size_t elem_bytes) {
+  if (elem_bytes == sizeof(double)) return hipMemcpy(dev, host, n * sizeof(double), hipMemcpyHostToDevice);
+  std::vector<float> f(n);
+  for (size_t i = 0; i < n; ++i) f[i] = float(host[i]);
+  return hipMemcpy(dev, f.data(), n * sizeof(float), hipMemcpyHostToDevice);
 }
 
 std::vector<double> transpose(const double* M, int rows, int cols) {
@@ -161,8 +173,14 @@ mlip_status mlip_create(const mlip_hparams* hp, const double* weights_host, size
   const int nin = (hp->lmax + 1) * k;
   ctx->n_enc = int(enc_tables(hp));
   ctx->n_head = int(head_tables(hp));
-  ctx->enc_stride = enc_table_doubles(k, hp->enc_hidden);
-  ctx->head_stride = head_table_doubles(nin, hp->reg_hidden);
+  ctx->enc_stride = enc_table_elems(k, hp->enc_hidden);
+  ctx->head_stride = head_table_elems(nin, hp->reg_hidden);
+  ctx->elem_bytes = hp->precision == 64 ? sizeof(double) : sizeof(float);
+  const int prec = hp->precision;
+  // encoder fragments per 16-byte load: hidden layers (8 output tiles) and
+  // output layer (k/16 tiles); the head keeps one fragment per load
+  const int vw_hid = int(16 / ctx->elem_bytes);
+  const int vw_out = std::min(vw_hid, k / 16);
 
   // encoder tables -> [w0 b0 | (fragments(W_t) b_t)... | fragments(W_out) b_out]
   std::vector<double> enc;
@@ -174,11 +192,11 @@ mlip_status mlip_create(const mlip_hparams* hp, const double* weights_host, size
     enc.insert(enc.end(), p, p + 2 * W);
     p += 2 * W;
     for (int h = 1; h < hp->enc_hidden; ++h) {
-      pack_fragments(p, kEncWidth, kEncWidth, &enc);
+      pack_fragments(p, kEncWidth, kEncWidth, prec, vw_hid, &enc);
       enc.insert(enc.end(), p + W * W, p + W * W + W);
       p += W * W + W;
     }
-    pack_fragments(p, k, kEncWidth, &enc);
+    pack_fragments(p, k, kEncWidth, prec, vw_out, &enc);
     enc.insert(enc.end(), p + size_t(k) * W, p + size_t(k) * W + k);
   }
   // head tables -> [frag(A0) | frag(A0^T) | c0 | (frag(A_t) frag(A_t^T) c_t)... | a_out c_out]
@@ -188,13 +206,13 @@ mlip_status mlip_create(const mlip_hparams* hp, const double* weights_host, size
   const int R = kHeadWidth;
   for (int t = 0; t < ctx->n_head; ++t) {
     const double* p = hsrc + size_t(t) * head_blob_doubles(hp);
-    pack_fragments(p, R, nin, &head);
-    pack_fragments(transpose(p, R, nin).data(), nin, R, &head);
+    pack_fragments(p, R, nin, prec, 1, &head);
+    pack_fragments(transpose(p, R, nin).data(), nin, R, prec, 1, &head);
     head.insert(head.end(), p + size_t(R) * nin, p + size_t(R) * nin + R);
     p += size_t(R) * nin + R;
     for (int h = 1; h < hp->reg_hidden; ++h) {
-      pack_fragments(p, R, R, &head);
-      pack_fragments(transpose(p, R, R).data(), R, R, &head);
+      pack_fragments(p, R, R, prec, 1, &head);
+      pack_fragments(transpose(p, R, R).data(), R, R, prec, 1, &head);
       head.insert(head.end(), p + R * R, p + R * R + R);
       p += R * R + R;
     }
@@ -209,9 +227,10 @@ mlip_status mlip_create(const mlip_hparams* hp, const double* weights_host, size
   }
   size_t cap = 0, cap2 = 0, cap3 = 0, cap4 = 0, cap5 = 0, cap6 = 0, cap7 = 0, cap8 = 0;
   mlip_status st = MLIP_OK;
-  if ((st = ensure(ctx, &ctx->d_enc, &cap, enc.size(), "encoder")) != MLIP_OK ||
-      (st = ensure(ctx, &ctx->d_head, &cap2, head.size(), "head")) != MLIP_OK ||
-      (st = ensure(ctx, &ctx->d_qc, &cap3, size_t(kAngRows * kMonomials), "tables")) != MLIP_OK ||
+  const size_t eb = ctx->elem_bytes;
+  if ((st = ensure(ctx, &ctx->d_enc, &cap, enc.size() * eb, "encoder")) != MLIP_OK ||
+      (st = ensure(ctx, &ctx->d_head, &cap2, head.size() * eb, "head")) != MLIP_OK ||
+      (st = ensure(ctx, &ctx->d_qc, &cap3, size_t(kAngRows * kMonomials) * eb, "tables")) != MLIP_OK ||
       (st = ensure(ctx, &ctx->d_totals, &cap4, size_t(16), "totals")) != MLIP_OK ||
       (st = ensure(ctx, &ctx->d_counters, &cap5, size_t(4), "counters")) != MLIP_OK ||
       (st = ensure(ctx, &ctx->d_flags, &cap6, size_t(4), "flags")) != MLIP_OK ||
@@ -220,9 +239,9 @@ mlip_status mlip_create(const mlip_hparams* hp, const double* weights_host, size
     mlip_destroy(ctx);
     return st;
   }
-  if (hipMemcpy(ctx->d_enc, enc.data(), enc.size() * sizeof(double), hipMemcpyHostToDevice) != hipSuccess ||
-      hipMemcpy(ctx->d_head, head.data(), head.size() * sizeof(double), hipMemcpyHostToDevice) != hipSuccess ||
-      hipMemcpy(ctx->d_qc, qc, sizeof(qc), hipMemcpyHostToDevice) != hipSuccess) {
+  if (upload(ctx->d_enc, enc.data(), enc.size(), eb) != hipSuccess ||
+      upload(ctx->d_head, head.data(), head.size(), eb) != hipSuccess ||
+      upload(ctx->d_qc, qc, size_t(kAngRows * kMonomials), eb) != hipSuccess) {
     (void)hipGetLastError();
     mlip_destroy(ctx);
     return MLIP_E_HIP;
@@ -332,8 +351,9 @@ mlip_status mlip_build_neighbors(mlip_ctx* ctx, int64_t n_atoms, const double* p
   ctx->n_tiles = tiles;
   ctx->n_blocks = int(std::max<int64_t>(1, std::min<int64_t>(tiles, ctx->n_cu)));
   const int64_t chunks = std::min<int64_t>(kChunkCap, (int64_t(T) * ctx->max_row + 15) / 16 + C);
-  const size_t slot = size_t(chunks) * 2 * size_t(ctx->hp.k) * 16;
-  MLIP_TRY(ensure(ctx, &ctx->d_ws, &ctx->cap_ws, slot * size_t(ctx->n_blocks), "workspace"));
+  ctx->ws_slot = size_t(chunks) * 2 * size_t(ctx->hp.k) * 16;
+  MLIP_TRY(ensure(ctx, &ctx->d_ws, &ctx->cap_ws, ctx->ws_slot * size_t(ctx->n_blocks) * ctx->elem_bytes,
+                  "workspace"));
   ctx->built = true;
   ctx->n_builds += 1;
   return MLIP_OK;
@@ -366,7 +386,7 @@ mlip_status mlip_compute(mlip_ctx* ctx, const double* pos_dev, double* energy_de
   a.totals = ctx->d_totals;
   a.counters = ctx->d_counters;
   a.ws = ctx->d_ws;
-  a.ws_slot = (long long)(ctx->cap_ws / size_t(ctx->n_blocks));
+  a.ws_slot = (long long)ctx->ws_slot;
   for (int d = 0; d < 3; ++d) {
     a.box[d] = ctx->box[d];
     a.inv_box[d] = 1.0 / ctx->box[d];
@@ -389,7 +409,7 @@ mlip_status mlip_compute(mlip_ctx* ctx, const double* pos_dev, double* energy_de
     a.tile_start[sp_i] = t;
     if (sp_i < a.C) t += (ctx->species_start[sp_i + 1] - ctx->species_start[sp_i] + ctx->tile_atoms - 1) / ctx->tile_atoms;
   }
-  if (ctx->n_tiles > 0) MLIP_HIP(ctx, launch_fused(ctx->hp.k, a, ctx->n_blocks, s));
+  if (ctx->n_tiles > 0) MLIP_HIP(ctx, launch_fused(ctx->hp.k, ctx->hp.precision, a, ctx->n_blocks, s));
   if (totals_host) {
     MLIP_HIP(ctx, hipMemcpyAsync(totals_host, ctx->d_totals, 10 * sizeof(double), hipMemcpyDeviceToHost, s));
     MLIP_HIP(ctx, hipStreamSynchronize(s));

@@ -10,12 +10,12 @@
 //      is cut into 16-pair chunks; all pairs of a chunk share one encoder
 //      table (pair conditioning, Section 3.2).
 //   B. Pass 1, one chunk per wavefront at a time: the radial encoder (Eq. 2)
-//      and its derivative in r run as float64 MFMA 16x16x4 products with the
+//      and its derivative in r run as MFMA 16x16x4 products with the
 //      16 pairs as one matrix dimension, the activation and its tangent
 //      stacked as two column tiles sharing every weight fragment.  The
 //      moment P_i = sum_j g_ang (x) g_rad (Eq. 4) is another MFMA product
 //      (K = pairs), accumulated into LDS.  The pre-cutoff output m and its
-//      tangent dm (2k doubles per pair) go to a fixed-size per-work-group
+//      tangent dm (2k values per pair) go to a fixed-size per-work-group
 //      workspace; nothing is recomputed in pass 2.
 //   C. Descriptor (Eq. 5), energy head (Eq. 6) and its gradient, and
 //      W_i = dE_i/dP_i (Eq. 7) for the tile's atoms, in LDS (W overwrites P).
@@ -25,20 +25,62 @@
 //      F_i += f_ij, w_i -= r_ij (x) f_ij (LDS atomics).
 //   E. Write E_i, w_i, add F_i; block-reduce totals.
 //
-// MFMA f64 16x16x4 register layout on gfx950 (lane = 16*g + c):
-//   A operand: lane holds A[c][g]; B operand: lane holds B[g][c];
-//   D/C: register q of lane holds D[4q + g][c].
-// A D-tile X can therefore feed a later product as B (contracting over its
-// rows, k-step q covers rows 4q..4q+3) or as A (X^T, same contraction).
+// The kernel is instantiated for two arithmetic types R of the network and
+// the contractions: float64 (the paper's evaluation precision, Section 4.1)
+// and float32 (the reduced-precision mode evaluated beside it, Sections 3.4
+// and 4.4).  Pair geometry (minimum image, r, unit vector, cutoff function)
+// and every output accumulation (F_i, F_j, w_i, E, totals) stay in float64
+// in both; the network, the angular features, the moment, W and the two
+// pass-2 contractions use R.
+//
+// MFMA 16x16x4 register layout on gfx950 (lane = 16*g + c), for both types:
+//   A operand: lane holds A[c][g]; B operand: lane holds B[g][c].
+// The result layout differs: register q of lane holds D[drow(q, g)][c] with
+// drow = 4q + g for float64 and 4g + q for float32.  A D-tile X can feed a
+// later product as B (contracting over its rows; k-step q covers rows
+// drow(q, 0..3)) or as A (X^T, same contraction); the host packs weight
+// fragments with the same row map.
 #include "mlip_internal.h"
 
 namespace mlip {
 namespace {
 
 typedef double v4d __attribute__((ext_vector_type(4)));
+typedef float v4f __attribute__((ext_vector_type(4)));
+
+template <typename R>
+struct Vec4;
+template <>
+struct Vec4<double> {
+  typedef v4d type;
+};
+template <>
+struct Vec4<float> {
+  typedef v4f type;
+};
+template <typename R>
+using v4 = typename Vec4<R>::type;
 
 __device__ __forceinline__ v4d mfma(double a, double b, v4d c) {
   return __builtin_amdgcn_mfma_f64_16x16x4f64(a, b, c, 0, 0, 0);
+}
+__device__ __forceinline__ v4f mfma(float a, float b, v4f c) {
+  return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+}
+
+// Result row held in register q of a lane of group g, and its inverse: row c
+// sits in register qof(c) of the lanes of group gof(c).
+template <typename R>
+__device__ __forceinline__ int drow(int q, int g) {
+  return sizeof(R) == 8 ? 4 * q + g : 4 * g + q;
+}
+template <typename R>
+__device__ __forceinline__ int qof(int c) {
+  return sizeof(R) == 8 ? c >> 2 : c & 3;
+}
+template <typename R>
+__device__ __forceinline__ int gof(int c) {
+  return sizeof(R) == 8 ? c & 3 : c >> 2;
 }
 
 // Logistic sigmoid 1 / (1 + exp(-z)) in float64, written out so the VALU
@@ -82,11 +124,22 @@ __device__ __forceinline__ double sigmoid(double z) {
   return y;
 }
 
+// Logistic sigmoid in float32 from the hardware base-2 exponential and
+// reciprocal (each within about one ulp).  For large -z the exponential
+// overflows to +inf and the reciprocal returns 0, the sigmoid's limit; for
+// large z it underflows to 0 and the result is 1.
+__device__ __forceinline__ float sigmoid(float z) {
+  constexpr float kLog2e = 1.44269504f;
+  const float e = __builtin_amdgcn_exp2f(-z * kLog2e);
+  return __builtin_amdgcn_rcpf(1.0f + e);
+}
+
 __device__ __forceinline__ double fold(double d, double L, double invL) { return d - L * rint(d * invL); }
 
 // Cartesian monomials of degree <= 3 in the order of the angular table.
-__device__ __forceinline__ void monomials(double x, double y, double z, double m[kMonomials]) {
-  m[0] = 1.0;
+template <typename R>
+__device__ __forceinline__ void monomials(R x, R y, R z, R m[kMonomials]) {
+  m[0] = R(1);
   m[1] = x; m[2] = y; m[3] = z;
   m[4] = x * x; m[5] = x * y; m[6] = x * z; m[7] = y * y; m[8] = y * z; m[9] = z * z;
   m[10] = x * x * x; m[11] = x * x * y; m[12] = x * x * z; m[13] = x * y * y; m[14] = x * y * z;
@@ -94,9 +147,10 @@ __device__ __forceinline__ void monomials(double x, double y, double z, double m
 }
 
 // Gradients of the monomials with respect to (x, y, z).
-__device__ __forceinline__ void monomial_grads(double x, double y, double z, double gx[kMonomials],
-                                               double gy[kMonomials], double gz[kMonomials]) {
-  const double xx = x * x, yy = y * y, zz = z * z;
+template <typename R>
+__device__ __forceinline__ void monomial_grads(R x, R y, R z, R gx[kMonomials], R gy[kMonomials],
+                                               R gz[kMonomials]) {
+  const R xx = x * x, yy = y * y, zz = z * z;
   gx[0] = 0; gy[0] = 0; gz[0] = 0;
   gx[1] = 1; gy[1] = 0; gz[1] = 0;
   gx[2] = 0; gy[2] = 1; gz[2] = 0;
@@ -119,13 +173,13 @@ __device__ __forceinline__ void monomial_grads(double x, double y, double z, dou
   gx[19] = 0; gy[19] = 0; gz[19] = 3 * zz;
 }
 
-template <int K, int TM>
+template <int K, int TM, typename R>
 struct Smem {
-  double P[TM][kAngRows][K + 1];  // moment, then its adjoint W (padded rows)
-  double xT[4 * K][16];           // head input vec(G), feature-major
-  double yT[kHeadWidth][16];      // head activations
-  double gT[kHeadWidth][16];      // head backward scratch
-  double qc[kAngRows][kMonomials];
+  R P[TM][kAngRows][K + 1];  // moment, then its adjoint W (padded rows)
+  R xT[4 * K][16];           // head input vec(G), feature-major
+  R yT[kHeadWidth][16];      // head activations
+  R gT[kHeadWidth][16];      // head backward scratch
+  R qc[kAngRows][kMonomials];
   double tpos[TM][3];
   double Fi[TM][3];
   double Wi[TM][9];
@@ -135,7 +189,7 @@ struct Smem {
   int orig[TM];
   int cnt[kMaxSpecies][TM];
   int base[kMaxSpecies][TM];
-  double l0[kMaxSpecies][2][kEncWidth];  // w0, b0 of the tile's encoder tables, by neighbour species
+  R l0[kMaxSpecies][2][kEncWidth];  // w0, b0 of the tile's encoder tables, by neighbour species
   int pair_j[kEntCap];
   unsigned char pair_a[kEntCap];
   int wsum[kWaves];
@@ -149,16 +203,14 @@ struct Smem {
   int na;
 };
 
-// Pass 1 on one chunk: encoder forward + tangent, moment accumulation and
-// the workspace write of (m, dm).
 // Position of the neighbour in column c of chunk ch (or a dummy), fetched
 // one chunk ahead so its latency overlaps the previous chunk's work.
 struct PairPos {
   double x, y, z;
 };
 
-template <int K, int TM>
-__device__ __forceinline__ PairPos load_pair_pos(const FusedArgs& A, const Smem<K, TM>& S, int ch) {
+template <int K, int TM, typename R>
+__device__ __forceinline__ PairPos load_pair_pos(const FusedArgs& A, const Smem<K, TM, R>& S, int ch) {
   const int c = threadIdx.x & 15;
   PairPos p{0.0, 0.0, 0.0};
   if (c < S.ch_count[ch]) {
@@ -172,127 +224,160 @@ __device__ __forceinline__ PairPos load_pair_pos(const FusedArgs& A, const Smem<
 
 // Pass 1 on one chunk: encoder forward + tangent, moment accumulation and
 // the workspace write of (m, dm).
-template <int K, int TM>
-__device__ void pass1_chunk(const FusedArgs& A, Smem<K, TM>& S, int ch, const PairPos pp,
-                            double* __restrict__ wsc) {
+template <int K, int TM, typename R>
+__device__ void pass1_chunk(const FusedArgs& A, Smem<K, TM, R>& S, int ch, const PairPos pp, R* __restrict__ wsc) {
   constexpr int KT = K / 16;
   const int lane = threadIdx.x & 63, g = lane >> 4, c = lane & 15;
   const int start = S.ch_start[ch], count = S.ch_count[ch];
   const int sj = S.ch_s[ch], si = S.tile_species;
   const int tau = A.enc_cond == 2 ? si * A.C + sj : (A.enc_cond == 1 ? sj : 0);
-  const double* __restrict__ tab = A.enc + (long long)tau * A.enc_stride;
+  const R* __restrict__ tab = static_cast<const R*>(A.enc) + (long long)tau * A.enc_stride;
 
-  // geometry of the pair in column c (Eq. 1)
+  // geometry of the pair in column c (Eq. 1), in float64
   const bool valid = c < count;
-  double ux = 1.0, uy = 0.0, uz = 0.0, r = 1.0, fc = 0.0;
+  double uxd = 1.0, uyd = 0.0, uzd = 0.0, rd = 1.0, fcd = 0.0;
   int atom = -1;
   if (valid) {
     atom = S.pair_a[start + c];
     const double dx = fold(pp.x - S.tpos[atom][0], A.box[0], A.inv_box[0]);
     const double dy = fold(pp.y - S.tpos[atom][1], A.box[1], A.inv_box[1]);
     const double dz = fold(pp.z - S.tpos[atom][2], A.box[2], A.inv_box[2]);
-    r = sqrt(dx * dx + dy * dy + dz * dz);
-    const double ir = 1.0 / r;
-    ux = dx * ir; uy = dy * ir; uz = dz * ir;
-    fc = 0.5 * (1.0 + cos(M_PI * r / A.rc));
+    rd = sqrt(dx * dx + dy * dy + dz * dz);
+    const double ir = 1.0 / rd;
+    uxd = dx * ir; uyd = dy * ir; uzd = dz * ir;
+    fcd = 0.5 * (1.0 + cos(M_PI * rd / A.rc));
+  }
+  const R r = R(rd), ux = R(uxd), uy = R(uyd), uz = R(uzd), fc = R(fcd);
+
+  // Weight fragments stream from L2 in 16-byte loads (VW fragments of
+  // consecutive output tiles per lane) through register rings, issued
+  // several k-steps ahead of the MFMAs that consume them.
+  constexpr int VW = 16 / int(sizeof(R));   // fragments per load
+  constexpr int NH = 8 / VW;                // loads per hidden-layer k-step
+  constexpr int VO = KT < VW ? KT : VW;     // fragments per output-layer load
+  constexpr int NO = KT / VO;               // loads per output-layer k-step
+  constexpr int kRing = sizeof(R) == 8 ? 3 : 4;
+  constexpr int kRingOut = sizeof(R) == 8 ? 3 : 6;
+  typedef R vh_t __attribute__((ext_vector_type(VW)));
+  typedef R vo_t __attribute__((ext_vector_type(VO)));
+  vh_t wb[kRing][NH];
+  vo_t wo[kRingOut][NO];
+  auto prefetch_hidden = [&](const R* L) {
+    const vh_t* __restrict__ f = reinterpret_cast<const vh_t*>(L) + lane;
+#pragma unroll
+    for (int p = 0; p < kRing - 1; ++p)
+#pragma unroll
+      for (int u = 0; u < NH; ++u) wb[p][u] = f[(p * NH + u) * 64];
+  };
+  auto prefetch_out = [&](const R* L) {
+    const vo_t* __restrict__ f = reinterpret_cast<const vo_t*>(L) + lane;
+#pragma unroll
+    for (int p = 0; p < kRingOut - 1; ++p)
+#pragma unroll
+      for (int u = 0; u < NO; ++u) wo[p][u] = f[(p * NO + u) * 64];
+  };
+  // float32 issues each product's first fragments before the activation
+  // work in front of it; float64 has no registers to spare for that
+  constexpr bool kEarly = sizeof(R) == 4;
+  const R* __restrict__ layer = tab + 2 * kEncWidth;
+  if (kEarly) {
+    if (A.enc_hidden > 1)
+      prefetch_hidden(layer);
+    else
+      prefetch_out(layer);
   }
 
-  // first layer (scalar input), rows in = 16T + 4i + g of column c
-  double h[8][4], dh[8][4];
+  // first layer (scalar input), rows in = 16T + drow(i, g) of column c
+  R h[8][4], dh[8][4];
 #pragma unroll
   for (int T = 0; T < 8; ++T)
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      const int in = 16 * T + 4 * i + g;
-      const double w0 = S.l0[sj][0][in], z = w0 * r + S.l0[sj][1][in];
-      const double s = sigmoid(z);
+      const int in = 16 * T + drow<R>(i, g);
+      const R w0 = S.l0[sj][0][in], z = w0 * r + S.l0[sj][1][in];
+      const R s = sigmoid(z);
       h[T][i] = z * s;
-      dh[T][i] = s * (1.0 + z * (1.0 - s)) * w0;
+      dh[T][i] = s * (R(1) + z * (R(1) - s)) * w0;
     }
 
   // residual hidden layers: Z = W H as 8 x 32 MFMA steps, forward and
   // tangent columns share each weight fragment
-  const double* __restrict__ layer = tab + 2 * kEncWidth;
   for (int t = 1; t < A.enc_hidden; ++t) {
-    const double* __restrict__ frag = layer + lane;
-    const double* __restrict__ bias = layer + kEncWidth * kEncWidth;
-    // the forward accumulators start from the bias (loaded with the first
-    // fragments, so its latency overlaps theirs); the tangent has none
-    v4d acc[8], dacc[8];
+    const vh_t* __restrict__ frag = reinterpret_cast<const vh_t*>(layer) + lane;
+    const R* __restrict__ bias = layer + kEncWidth * kEncWidth;
+    if (!kEarly) prefetch_hidden(layer);
+    // the forward accumulators start from the bias; the tangent has none
+    v4<R> acc[8], dacc[8];
 #pragma unroll
     for (int To = 0; To < 8; ++To) {
-      acc[To] = v4d{bias[16 * To + g], bias[16 * To + 4 + g], bias[16 * To + 8 + g], bias[16 * To + 12 + g]};
-      dacc[To] = v4d{0, 0, 0, 0};
+      acc[To] = v4<R>{bias[16 * To + drow<R>(0, g)], bias[16 * To + drow<R>(1, g)], bias[16 * To + drow<R>(2, g)],
+                      bias[16 * To + drow<R>(3, g)]};
+      dacc[To] = v4<R>{0, 0, 0, 0};
     }
-    // weight fragments stream from L2 through a 3-deep register ring,
-    // issued two k-steps ahead of the MFMAs that consume them
-    constexpr int kRing = 3;  // fragments issued kRing-1 k-steps ahead
-    double wb[kRing][8];
-#pragma unroll
-    for (int pre = 0; pre < kRing - 1; ++pre)
-#pragma unroll
-      for (int To = 0; To < 8; ++To) wb[pre][To] = frag[(pre * 8 + To) * 64];
 #pragma unroll
     for (int ks = 0; ks < 32; ++ks) {
       if (ks + kRing - 1 < 32) {
 #pragma unroll
-        for (int To = 0; To < 8; ++To) wb[(ks + kRing - 1) % kRing][To] = frag[((ks + kRing - 1) * 8 + To) * 64];
+        for (int u = 0; u < NH; ++u) wb[(ks + kRing - 1) % kRing][u] = frag[((ks + kRing - 1) * NH + u) * 64];
       }
       __builtin_amdgcn_sched_barrier(0);
       const int T = ks >> 2, i = ks & 3;
 #pragma unroll
       for (int To = 0; To < 8; ++To) {
-        acc[To] = mfma(wb[ks % kRing][To], h[T][i], acc[To]);
-        dacc[To] = mfma(wb[ks % kRing][To], dh[T][i], dacc[To]);
+        const R wv = wb[ks % kRing][To / VW][To % VW];
+        acc[To] = mfma(wv, h[T][i], acc[To]);
+        dacc[To] = mfma(wv, dh[T][i], dacc[To]);
       }
       __builtin_amdgcn_sched_barrier(0);
+    }
+    layer += kEncWidth * kEncWidth + kEncWidth;
+    if (kEarly) {
+      if (t + 1 < A.enc_hidden)
+        prefetch_hidden(layer);
+      else
+        prefetch_out(layer);
     }
 #pragma unroll
     for (int To = 0; To < 8; ++To)
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
-        const double z = acc[To][q];
-        const double s = sigmoid(z);
+        const R z = acc[To][q];
+        const R s = sigmoid(z);
         h[To][q] += z * s;
-        dh[To][q] += s * (1.0 + z * (1.0 - s)) * dacc[To][q];
+        dh[To][q] += s * (R(1) + z * (R(1) - s)) * dacc[To][q];
       }
-    layer += kEncWidth * kEncWidth + kEncWidth;
   }
 
-  // output layer with pairs as rows: m[pair 4q+g][16Tc + c]; even and odd
-  // k-steps accumulate separately so 4 KT independent MFMA chains are in
+  // output layer with pairs as rows: m[pair drow(q, g)][16Tc + c]; even and
+  // odd k-steps accumulate separately so 4 KT independent MFMA chains are in
   // flight
-  v4d mo[KT], dmo[KT];
+  v4<R> mo[KT], dmo[KT];
   {
-    const double* __restrict__ bout = layer + K * kEncWidth;
-    v4d mo2[2][KT], dmo2[2][KT];
+    const R* __restrict__ bout = layer + K * kEncWidth;
+    v4<R> mo2[2][KT], dmo2[2][KT];
 #pragma unroll
     for (int Tc = 0; Tc < KT; ++Tc) {
-      const double b = bout[16 * Tc + c];
-      mo2[0][Tc] = v4d{b, b, b, b};
-      mo2[1][Tc] = v4d{0, 0, 0, 0};
-      dmo2[0][Tc] = v4d{0, 0, 0, 0};
-      dmo2[1][Tc] = v4d{0, 0, 0, 0};
+      const R b = bout[16 * Tc + c];
+      mo2[0][Tc] = v4<R>{b, b, b, b};
+      mo2[1][Tc] = v4<R>{0, 0, 0, 0};
+      dmo2[0][Tc] = v4<R>{0, 0, 0, 0};
+      dmo2[1][Tc] = v4<R>{0, 0, 0, 0};
     }
-    const double* __restrict__ frag = layer + lane;
-    double wb[3][KT];
-#pragma unroll
-    for (int Tc = 0; Tc < KT; ++Tc) {
-      wb[0][Tc] = frag[(0 * KT + Tc) * 64];
-      wb[1][Tc] = frag[(1 * KT + Tc) * 64];
-    }
+    if (!kEarly) prefetch_out(layer);
+    const vo_t* __restrict__ frag = reinterpret_cast<const vo_t*>(layer) + lane;
 #pragma unroll
     for (int ks = 0; ks < 32; ++ks) {
-      if (ks + 2 < 32) {
+      if (ks + kRingOut - 1 < 32) {
 #pragma unroll
-        for (int Tc = 0; Tc < KT; ++Tc) wb[(ks + 2) % 3][Tc] = frag[((ks + 2) * KT + Tc) * 64];
+        for (int u = 0; u < NO; ++u) wo[(ks + kRingOut - 1) % kRingOut][u] = frag[((ks + kRingOut - 1) * NO + u) * 64];
       }
       __builtin_amdgcn_sched_barrier(0);
       const int T = ks >> 2, i = ks & 3;
 #pragma unroll
       for (int Tc = 0; Tc < KT; ++Tc) {
-        mo2[ks & 1][Tc] = mfma(h[T][i], wb[ks % 3][Tc], mo2[ks & 1][Tc]);
-        dmo2[ks & 1][Tc] = mfma(dh[T][i], wb[ks % 3][Tc], dmo2[ks & 1][Tc]);
+        const R wv = wo[ks % kRingOut][Tc / VO][Tc % VO];
+        mo2[ks & 1][Tc] = mfma(h[T][i], wv, mo2[ks & 1][Tc]);
+        dmo2[ks & 1][Tc] = mfma(dh[T][i], wv, dmo2[ks & 1][Tc]);
       }
       __builtin_amdgcn_sched_barrier(0);
     }
@@ -306,45 +391,46 @@ __device__ void pass1_chunk(const FusedArgs& A, Smem<K, TM>& S, int ch, const Pa
   // moment: P[mm][col] += sum_pairs fc * a_mm(u) * m[pair][col], one MFMA
   // product per centre atom present in the chunk (pairs of other atoms are
   // masked to zero in the A operand)
-  double av[4];
+  R av[4];
   int aa[4];
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
-    const int src = 4 * q + g;  // pair index; any lane with c == src holds it
-    const double px = __shfl(ux, src, 64), py = __shfl(uy, src, 64), pz = __shfl(uz, src, 64);
-    const double pf = __shfl(fc, src, 64);
+    const int src = drow<R>(q, g);  // pair index; any lane with c == src holds it
+    const R px = __shfl(ux, src, 64), py = __shfl(uy, src, 64), pz = __shfl(uz, src, 64);
+    const R pf = __shfl(fc, src, 64);
     aa[q] = __shfl(atom, src, 64);
-    double mono[kMonomials];
+    R mono[kMonomials];
     monomials(px, py, pz, mono);
-    double s = 0.0;
+    R s = 0;
 #pragma unroll
     for (int m = 0; m < kMonomials; ++m) s += S.qc[c][m] * mono[m];
     av[q] = pf * s;
   }
   const int a_first = S.pair_a[start], a_last = S.pair_a[start + count - 1];
   for (int a = a_first; a <= a_last; ++a) {
-    v4d pacc[KT];
+    v4<R> pacc[KT];
 #pragma unroll
-    for (int Tc = 0; Tc < KT; ++Tc) pacc[Tc] = v4d{0, 0, 0, 0};
+    for (int Tc = 0; Tc < KT; ++Tc) pacc[Tc] = v4<R>{0, 0, 0, 0};
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
-      const double av_a = aa[q] == a ? av[q] : 0.0;
+      const R av_a = aa[q] == a ? av[q] : R(0);
 #pragma unroll
       for (int Tc = 0; Tc < KT; ++Tc) pacc[Tc] = mfma(av_a, mo[Tc][q], pacc[Tc]);
     }
 #pragma unroll
     for (int Tc = 0; Tc < KT; ++Tc)
 #pragma unroll
-      for (int q = 0; q < 4; ++q) atomicAdd(&S.P[a][4 * q + g][16 * Tc + c], pacc[Tc][q]);
+      for (int q = 0; q < 4; ++q) atomicAdd(&S.P[a][drow<R>(q, g)][16 * Tc + c], pacc[Tc][q]);
   }
 
-  // workspace in the B-operand layout pass 2 loads: block (Tc, i) holds
-  // m[c' = 16Tc + 4i + g'][pair c'] at lane 16 g' + c'
+  // workspace in the B-operand order pass 2 loads, contiguous per lane:
+  // lane 16 g' + c' holds m[pair c'][16Tc + drow(i, g')] at 4 KT lane' +
+  // 4 Tc + i (then the same for dm)
 #pragma unroll
   for (int Tc = 0; Tc < KT; ++Tc)
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
-      const int off = (Tc * 4 + (c >> 2)) * 64 + 16 * (c & 3) + 4 * q + g;
+      const int off = (16 * gof<R>(c) + drow<R>(q, g)) * (4 * KT) + Tc * 4 + qof<R>(c);
       wsc[off] = mo[Tc][q];
       wsc[K * 16 + off] = dmo[Tc][q];
     }
@@ -352,29 +438,40 @@ __device__ void pass1_chunk(const FusedArgs& A, Smem<K, TM>& S, int ch, const Pa
 
 // Inputs of pass 2 for one chunk: the workspace tiles (m, dm) in B-operand
 // order and the neighbour position; loaded one chunk ahead.
-template <int K>
+template <int K, typename R>
 struct Pass2In {
-  double mB[K / 16][4], dmB[K / 16][4];
+  R mB[K / 16][4], dmB[K / 16][4];
   PairPos pp;
 };
 
-template <int K, int TM>
-__device__ __forceinline__ void pass2_load(const FusedArgs& A, const Smem<K, TM>& S, int ch,
-                                           const double* __restrict__ wsc, Pass2In<K>& in) {
+template <int K, int TM, typename R>
+__device__ __forceinline__ void pass2_load(const FusedArgs& A, const Smem<K, TM, R>& S, int ch,
+                                           const R* __restrict__ wsc, Pass2In<K, R>& in) {
+  constexpr int VW = 16 / int(sizeof(R));
+  constexpr int NV = K / 4 / VW;  // 16-byte loads per lane for m (and for dm)
+  typedef R vw_t __attribute__((ext_vector_type(VW)));
   const int lane = threadIdx.x & 63;
+  const vw_t* __restrict__ pm = reinterpret_cast<const vw_t*>(wsc + lane * (K / 4));
+  const vw_t* __restrict__ pd = reinterpret_cast<const vw_t*>(wsc + K * 16 + lane * (K / 4));
+  vw_t vm[NV], vd[NV];
+#pragma unroll
+  for (int v = 0; v < NV; ++v) {
+    vm[v] = pm[v];
+    vd[v] = pd[v];
+  }
 #pragma unroll
   for (int Tc = 0; Tc < K / 16; ++Tc)
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      in.mB[Tc][i] = wsc[(Tc * 4 + i) * 64 + lane];
-      in.dmB[Tc][i] = wsc[K * 16 + (Tc * 4 + i) * 64 + lane];
+      in.mB[Tc][i] = vm[(Tc * 4 + i) / VW][(Tc * 4 + i) % VW];
+      in.dmB[Tc][i] = vd[(Tc * 4 + i) / VW][(Tc * 4 + i) % VW];
     }
   in.pp = load_pair_pos(A, S, ch);
 }
 
 // Pass 2 on one chunk: W contractions, partial forces and scatter.
-template <int K, int TM>
-__device__ void pass2_chunk(const FusedArgs& A, Smem<K, TM>& S, int ch, const Pass2In<K>& in) {
+template <int K, int TM, typename R>
+__device__ void pass2_chunk(const FusedArgs& A, Smem<K, TM, R>& S, int ch, const Pass2In<K, R>& in) {
   constexpr int KT = K / 16;
   const int lane = threadIdx.x & 63, g = lane >> 4, c = lane & 15;
   const int start = S.ch_start[ch], count = S.ch_count[ch];
@@ -394,19 +491,19 @@ __device__ void pass2_chunk(const FusedArgs& A, Smem<K, TM>& S, int ch, const Pa
   const double ir = 1.0 / r;
   const double ux = dx * ir, uy = dy * ir, uz = dz * ir;
   const double arg = M_PI * r / A.rc;
-  const double fc = valid ? 0.5 * (1.0 + cos(arg)) : 0.0;
-  const double dfc = valid ? -0.5 * M_PI / A.rc * sin(arg) : 0.0;
+  const R fc = valid ? R(0.5 * (1.0 + cos(arg))) : R(0);
+  const R dfc = valid ? R(-0.5 * M_PI / A.rc * sin(arg)) : R(0);
 
   // (W m) and (W dm) for this column's own centre atom
-  v4d wm = v4d{0, 0, 0, 0}, wdm = v4d{0, 0, 0, 0};
+  v4<R> wm = v4<R>{0, 0, 0, 0}, wdm = v4<R>{0, 0, 0, 0};
   const int a_first = S.pair_a[start], a_last = S.pair_a[start + count - 1];
   for (int a = a_first; a <= a_last; ++a) {
-    v4d t1 = v4d{0, 0, 0, 0}, t2 = v4d{0, 0, 0, 0};
+    v4<R> t1 = v4<R>{0, 0, 0, 0}, t2 = v4<R>{0, 0, 0, 0};
 #pragma unroll
     for (int Tc = 0; Tc < KT; ++Tc)
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const double w = S.P[a][c][16 * Tc + 4 * i + g];
+        const R w = S.P[a][c][16 * Tc + drow<R>(i, g)];
         t1 = mfma(w, in.mB[Tc][i], t1);
         t2 = mfma(w, in.dmB[Tc][i], t2);
       }
@@ -416,25 +513,25 @@ __device__ void pass2_chunk(const FusedArgs& A, Smem<K, TM>& S, int ch, const Pa
     }
   }
 
-  // angular features a_mm and gradients for rows mm = 4q + g of this pair
-  double mono[kMonomials], gx[kMonomials], gy[kMonomials], gz[kMonomials];
-  monomials(ux, uy, uz, mono);
-  monomial_grads(ux, uy, uz, gx, gy, gz);
-  double s = 0.0, tx = 0.0, ty = 0.0, tz = 0.0;
+  // angular features a_mm and gradients for rows mm = drow(q, g) of this pair
+  R mono[kMonomials], gx[kMonomials], gy[kMonomials], gz[kMonomials];
+  monomials(R(ux), R(uy), R(uz), mono);
+  monomial_grads(R(ux), R(uy), R(uz), gx, gy, gz);
+  R s = 0, tx = 0, ty = 0, tz = 0;
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
-    const int mm = 4 * q + g;
-    double a_v = 0.0, a_x = 0.0, a_y = 0.0, a_z = 0.0;
+    const int mm = drow<R>(q, g);
+    R a_v = 0, a_x = 0, a_y = 0, a_z = 0;
 #pragma unroll
     for (int m = 0; m < kMonomials; ++m) {
-      const double co = S.qc[mm][m];
+      const R co = S.qc[mm][m];
       a_v += co * mono[m];
       a_x += co * gx[m];
       a_y += co * gy[m];
       a_z += co * gz[m];
     }
-    const double v = fc * wm[q];                      // v = W g
-    const double wg = dfc * wm[q] + fc * wdm[q];      // W g'
+    const R v = fc * wm[q];                   // v = W g
+    const R wg = dfc * wm[q] + fc * wdm[q];   // W g'
     s += a_v * wg;
     tx += a_x * v;
     ty += a_y * v;
@@ -447,11 +544,12 @@ __device__ void pass2_chunk(const FusedArgs& A, Smem<K, TM>& S, int ch, const Pa
     ty += __shfl_xor(ty, o, 64);
     tz += __shfl_xor(tz, o, 64);
   }
-  // f = s u + (I - u u^T) t / r  (Eq. 10, reassociated)
-  const double ut = ux * tx + uy * ty + uz * tz;
-  const double fx = s * ux + (tx - ut * ux) * ir;
-  const double fy = s * uy + (ty - ut * uy) * ir;
-  const double fz = s * uz + (tz - ut * uz) * ir;
+  // f = s u + (I - u u^T) t / r  (Eq. 10, reassociated), in float64
+  const double sd = s, txd = tx, tyd = ty, tzd = tz;
+  const double ut = ux * txd + uy * tyd + uz * tzd;
+  const double fx = sd * ux + (txd - ut * ux) * ir;
+  const double fy = sd * uy + (tyd - ut * uy) * ir;
+  const double fz = sd * uz + (tzd - ut * uz) * ir;
   if (valid) {
     if (g == 0) {
       atomicAdd(&A.forces[3 * (long long)j], -fx);
@@ -482,17 +580,17 @@ __device__ void pass2_chunk(const FusedArgs& A, Smem<K, TM>& S, int ch, const Pa
 // Activations live in LDS feature-major ([feature][atom]) so that B-operand
 // reads are contiguous; pre-activations stay in registers for the backward
 // pass.
-template <int K, int TM>
-__device__ void head_stage(const FusedArgs& A, Smem<K, TM>& S) {
-  constexpr int R = kHeadWidth;
-  constexpr int HS = 2 * R * R + R;  // one hidden layer: A_t and A_t^T fragments, c_t
+template <int K, int TM, typename R>
+__device__ void head_stage(const FusedArgs& A, Smem<K, TM, R>& S) {
+  constexpr int RW = kHeadWidth;
+  constexpr int HS = 2 * RW * RW + RW;  // one hidden layer: A_t and A_t^T fragments, c_t
   const int tid = threadIdx.x, lane = tid & 63, g = lane >> 4, c = lane & 15, w = tid >> 6;
   const int na = S.na;
   const int nin = (A.lmax + 1) * K;
   const int tin = nin / 16;
   for (int u = tid; u < 16 * nin; u += kThreads) {
     const int a = u & 15, in = u >> 4;
-    double v = 0.0;
+    R v = 0;
     if (a < na) {
       const int l = in / K, col = in % K;
       if (l == 0) {
@@ -506,98 +604,104 @@ __device__ void head_stage(const FusedArgs& A, Smem<K, TM>& S) {
   __syncthreads();
 
   const int rho = A.reg_cond ? S.tile_species : 0;
-  const double* __restrict__ A0f = A.head + (long long)rho * A.head_stride;  // A0 fragments
-  const double* __restrict__ A0Tf = A0f + R * nin;                          // A0^T fragments
-  const double* __restrict__ c0 = A0Tf + R * nin;
-  const double* __restrict__ hid = c0 + R;
-  const double* __restrict__ aout = hid + (A.reg_hidden - 1) * HS;
-  const int r0 = 16 * w + g;  // this lane's rows are r0 + 4q
+  const R* __restrict__ A0f = static_cast<const R*>(A.head) + (long long)rho * A.head_stride;  // A0 fragments
+  const R* __restrict__ A0Tf = A0f + RW * nin;                                               // A0^T fragments
+  const R* __restrict__ c0 = A0Tf + RW * nin;
+  const R* __restrict__ hid = c0 + RW;
+  const R* __restrict__ aout = hid + (A.reg_hidden - 1) * HS;
+  // this lane's result rows are 16 w + drow(q, g)
+#define ROW(q) (16 * w + drow<R>(q, g))
 
   // layer 0: z0 = A0 x + c0
-  v4d z0 = v4d{c0[r0], c0[r0 + 4], c0[r0 + 8], c0[r0 + 12]};
+  v4<R> z0 = v4<R>{c0[ROW(0)], c0[ROW(1)], c0[ROW(2)], c0[ROW(3)]};
   for (int ks = 0; ks < nin / 4; ++ks)
-    z0 = mfma(A0f[(ks * 4 + w) * 64 + lane], S.xT[16 * (ks >> 2) + 4 * (ks & 3) + g][c], z0);
+    z0 = mfma(A0f[(ks * 4 + w) * 64 + lane], S.xT[16 * (ks >> 2) + drow<R>(ks & 3, g)][c], z0);
 #pragma unroll
-  for (int q = 0; q < 4; ++q) S.yT[r0 + 4 * q][c] = z0[q] * sigmoid(z0[q]);
+  for (int q = 0; q < 4; ++q) S.yT[ROW(q)][c] = z0[q] * sigmoid(z0[q]);
   __syncthreads();
 
   // residual layers: y <- y + silu(A_t y + c_t)
-  v4d zeta[kMaxHidden];
+  v4<R> zeta[kMaxHidden];
 #pragma unroll
   for (int t = 1; t < kMaxHidden; ++t) {
     if (t >= A.reg_hidden) break;
-    const double* __restrict__ Af = hid + (t - 1) * HS;
-    const double* __restrict__ ct = Af + 2 * R * R;
-    v4d z = v4d{ct[r0], ct[r0 + 4], ct[r0 + 8], ct[r0 + 12]};
+    const R* __restrict__ Af = hid + (t - 1) * HS;
+    const R* __restrict__ ct = Af + 2 * RW * RW;
+    v4<R> z = v4<R>{ct[ROW(0)], ct[ROW(1)], ct[ROW(2)], ct[ROW(3)]};
 #pragma unroll
-    for (int ks = 0; ks < 16; ++ks) z = mfma(Af[(ks * 4 + w) * 64 + lane], S.yT[16 * (ks >> 2) + 4 * (ks & 3) + g][c], z);
+    for (int ks = 0; ks < 16; ++ks)
+      z = mfma(Af[(ks * 4 + w) * 64 + lane], S.yT[16 * (ks >> 2) + drow<R>(ks & 3, g)][c], z);
     zeta[t] = z;
     __syncthreads();
 #pragma unroll
-    for (int q = 0; q < 4; ++q) S.yT[r0 + 4 * q][c] += z[q] * sigmoid(z[q]);
+    for (int q = 0; q < 4; ++q) S.yT[ROW(q)][c] += z[q] * sigmoid(z[q]);
     __syncthreads();
   }
   if (tid < na) {
-    double e = aout[R];
-    for (int o = 0; o < R; ++o) e += aout[o] * S.yT[o][tid];
-    S.Ei[tid] = e;
+    R e = aout[RW];
+    for (int o = 0; o < RW; ++o) e += aout[o] * S.yT[o][tid];
+    S.Ei[tid] = double(e);
   }
 
   // backward: d <- d + A_t^T (silu'(zeta_t) d), starting from d = a_out
-  v4d d = v4d{aout[r0], aout[r0 + 4], aout[r0 + 8], aout[r0 + 12]};
+  v4<R> d = v4<R>{aout[ROW(0)], aout[ROW(1)], aout[ROW(2)], aout[ROW(3)]};
 #pragma unroll
   for (int t = kMaxHidden - 1; t >= 1; --t) {
     if (t >= A.reg_hidden) continue;
-    const double* __restrict__ ATf = hid + (t - 1) * HS + R * R;
+    const R* __restrict__ ATf = hid + (t - 1) * HS + RW * RW;
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
-      const double z = zeta[t][q], sg = sigmoid(z);
-      S.gT[r0 + 4 * q][c] = sg * (1.0 + z * (1.0 - sg)) * d[q];
+      const R z = zeta[t][q], sg = sigmoid(z);
+      S.gT[ROW(q)][c] = sg * (R(1) + z * (R(1) - sg)) * d[q];
     }
     __syncthreads();
-    v4d acc = v4d{0, 0, 0, 0};
+    v4<R> acc = v4<R>{0, 0, 0, 0};
 #pragma unroll
-    for (int ks = 0; ks < 16; ++ks) acc = mfma(ATf[(ks * 4 + w) * 64 + lane], S.gT[16 * (ks >> 2) + 4 * (ks & 3) + g][c], acc);
+    for (int ks = 0; ks < 16; ++ks)
+      acc = mfma(ATf[(ks * 4 + w) * 64 + lane], S.gT[16 * (ks >> 2) + drow<R>(ks & 3, g)][c], acc);
     d += acc;
     __syncthreads();
   }
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
-    const double z = z0[q], sg = sigmoid(z);
-    S.gT[r0 + 4 * q][c] = sg * (1.0 + z * (1.0 - sg)) * d[q];
+    const R z = z0[q], sg = sigmoid(z);
+    S.gT[ROW(q)][c] = sg * (R(1) + z * (R(1) - sg)) * d[q];
   }
   __syncthreads();
   // dE/dx = A0^T g0, then W[0][col] = dE/dG[0][col], W[m][col] = 2 dE/dG[l][col] P[m][col]
   for (int tt = w; tt < tin; tt += kWaves) {
-    v4d acc = v4d{0, 0, 0, 0};
+    v4<R> acc = v4<R>{0, 0, 0, 0};
 #pragma unroll
-    for (int ks = 0; ks < 16; ++ks) acc = mfma(A0Tf[(ks * tin + tt) * 64 + lane], S.gT[16 * (ks >> 2) + 4 * (ks & 3) + g][c], acc);
+    for (int ks = 0; ks < 16; ++ks)
+      acc = mfma(A0Tf[(ks * tin + tt) * 64 + lane], S.gT[16 * (ks >> 2) + drow<R>(ks & 3, g)][c], acc);
     if (c < na) {
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
-        const int in = 16 * tt + 4 * q + g;
+        const int in = 16 * tt + drow<R>(q, g);
         const int l = in / K, col = in % K;
         if (l == 0) {
           S.P[c][0][col] = acc[q];
         } else {
-          for (int mm = l * l; mm < (l + 1) * (l + 1); ++mm) S.P[c][mm][col] *= 2.0 * acc[q];
+          for (int mm = l * l; mm < (l + 1) * (l + 1); ++mm) S.P[c][mm][col] *= R(2) * acc[q];
         }
       }
     }
   }
   __syncthreads();
+#undef ROW
 }
 
-template <int K, int TM>
+template <int K, int TM, typename R>
 __global__ __launch_bounds__(kThreads, 1) void k_fused(FusedArgs A) {
   extern __shared__ __align__(16) unsigned char smem_raw[];
-  Smem<K, TM>& S = *reinterpret_cast<Smem<K, TM>*>(smem_raw);
+  Smem<K, TM, R>& S = *reinterpret_cast<Smem<K, TM, R>*>(smem_raw);
   const int tid = threadIdx.x, wave = tid >> 6;
-  constexpr int KT = K / 16;
-  const long long chunk_doubles = 2LL * K * 16;
-  double* __restrict__ ws_slot = A.ws + (long long)blockIdx.x * A.ws_slot;
+  const long long chunk_elems = 2LL * K * 16;
+  R* __restrict__ ws_slot = static_cast<R*>(A.ws) + (long long)blockIdx.x * A.ws_slot;
+  const R* __restrict__ enc = static_cast<const R*>(A.enc);
+  const R* __restrict__ qc = static_cast<const R*>(A.qc);
 
-  for (int u = tid; u < kAngRows * kMonomials; u += kThreads) S.qc[u / kMonomials][u % kMonomials] = A.qc[u];
+  for (int u = tid; u < kAngRows * kMonomials; u += kThreads) S.qc[u / kMonomials][u % kMonomials] = qc[u];
 
   // XCD-aware assignment: blocks are dispatched round-robin over the 8 XCDs,
   // so block b works on the b%8-th contiguous eighth of the tile list and
@@ -629,7 +733,7 @@ __global__ __launch_bounds__(kThreads, 1) void k_fused(FusedArgs A) {
       const int sj = u / (2 * kEncWidth), rem = u % (2 * kEncWidth);
       const int si = S.tile_species;
       const int tau = A.enc_cond == 2 ? si * A.C + sj : (A.enc_cond == 1 ? sj : 0);
-      S.l0[sj][rem / kEncWidth][rem % kEncWidth] = A.enc[(long long)tau * A.enc_stride + rem];
+      S.l0[sj][rem / kEncWidth][rem % kEncWidth] = enc[(long long)tau * A.enc_stride + rem];
     }
     if (tid <= TM) {
       const int k = tid < na ? tid : na;
@@ -651,7 +755,7 @@ __global__ __launch_bounds__(kThreads, 1) void k_fused(FusedArgs A) {
       S.Ei[tid] = 0.0;
     }
     for (int u = tid; u < kMaxSpecies * TM; u += kThreads) S.cnt[u / TM][u % TM] = 0;
-    for (int u = tid; u < TM * kAngRows * (K + 1); u += kThreads) (&S.P[0][0][0])[u] = 0.0;
+    for (int u = tid; u < TM * kAngRows * (K + 1); u += kThreads) (&S.P[0][0][0])[u] = R(0);
     __syncthreads();
     const int nent = S.ent_base[na];
     const long long ebase = S.row_beg[0];
@@ -751,22 +855,22 @@ __global__ __launch_bounds__(kThreads, 1) void k_fused(FusedArgs A) {
       for (int ch = wave; ch < nch; ch += kWaves) {
         const PairPos cur = next;
         if (ch + kWaves < nch) next = load_pair_pos(A, S, ch + kWaves);
-        pass1_chunk<K, TM>(A, S, ch, cur, ws_slot + ch * chunk_doubles);
+        pass1_chunk<K, TM, R>(A, S, ch, cur, ws_slot + ch * chunk_elems);
       }
     }
     __syncthreads();
 
     // ---- C: descriptor, head, W ------------------------------------------
-    head_stage<K, TM>(A, S);
+    head_stage<K, TM, R>(A, S);
 
     // ---- D: pass 2 ---------------------------------------------------------
     {
-      Pass2In<K> next;
-      if (wave < nch) pass2_load(A, S, wave, ws_slot + wave * chunk_doubles, next);
+      Pass2In<K, R> next;
+      if (wave < nch) pass2_load(A, S, wave, ws_slot + wave * chunk_elems, next);
       for (int ch = wave; ch < nch; ch += kWaves) {
-        const Pass2In<K> cur = next;
-        if (ch + kWaves < nch) pass2_load(A, S, ch + kWaves, ws_slot + (ch + kWaves) * chunk_doubles, next);
-        pass2_chunk<K, TM>(A, S, ch, cur);
+        const Pass2In<K, R> cur = next;
+        if (ch + kWaves < nch) pass2_load(A, S, ch + kWaves, ws_slot + (ch + kWaves) * chunk_elems, next);
+        pass2_chunk<K, TM, R>(A, S, ch, cur);
       }
     }
     __syncthreads();
@@ -803,38 +907,29 @@ __global__ __launch_bounds__(kThreads, 1) void k_fused(FusedArgs A) {
       if (tid == 0) atomicAdd(&A.counters[0], (unsigned long long)S.n_active);
     }
     __syncthreads();
-    (void)KT;
   }
 }
 
-template <int K, int TM>
+template <int K, int TM, typename R>
 hipError_t launch_k(const FusedArgs& a, int n_blocks, hipStream_t s) {
-  const size_t smem = sizeof(Smem<K, TM>);
+  const size_t smem = sizeof(Smem<K, TM, R>);
   static bool attr_set = false;
   if (!attr_set) {
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_fused<K, TM>),
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_fused<K, TM, R>),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, int(smem));
     if (e != hipSuccess) return e;
     attr_set = true;
   }
-  k_fused<K, TM><<<dim3(unsigned(n_blocks)), dim3(kThreads), smem, s>>>(a);
+  k_fused<K, TM, R><<<dim3(unsigned(n_blocks)), dim3(kThreads), smem, s>>>(a);
   return hipGetLastError();
 }
 
 }  // namespace
 
-size_t fused_smem_bytes(int k) {
-  switch (k) {
-    case 32: return sizeof(Smem<32, kTileMax>);
-    default: return 0;
-  }
-}
-
-hipError_t launch_fused(int k, const FusedArgs& a, int n_blocks, hipStream_t s) {
-  switch (k) {
-    case 32: return launch_k<32, kTileMax>(a, n_blocks, s);
-    default: return hipErrorInvalidValue;
-  }
+hipError_t launch_fused(int k, int precision, const FusedArgs& a, int n_blocks, hipStream_t s) {
+  if (k == 32 && precision == 64) return launch_k<32, kTileMax, double>(a, n_blocks, s);
+  if (k == 32 && precision == 32) return launch_k<32, kTileMax, float>(a, n_blocks, s);
+  return hipErrorInvalidValue;
 }
 
 }  // namespace mlip

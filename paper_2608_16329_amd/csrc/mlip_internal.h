@@ -25,13 +25,13 @@ constexpr int kMaxHidden = 8;             // hidden layers supported on the GPU 
 constexpr int kAngRows = 16;              // angular rows, (lmax+1)^2 <= 16
 constexpr int kMonomials = 20;            // Cartesian monomials of degree <= 3
 
-// Number of float64 in one packed encoder table (device layout).
-inline size_t enc_table_doubles(int k, int enc_hidden) {
+// Number of values in one packed encoder table (device layout).
+inline size_t enc_table_elems(int k, int enc_hidden) {
   return 2 * kEncWidth + size_t(enc_hidden - 1) * (kEncWidth * kEncWidth + kEncWidth) +
          size_t(k) * kEncWidth + k;
 }
-// Number of float64 in one packed head table (device layout).
-inline size_t head_table_doubles(int nin, int reg_hidden) {
+// Number of values in one packed head table (device layout).
+inline size_t head_table_elems(int nin, int reg_hidden) {
   return 2 * size_t(kHeadWidth) * nin + kHeadWidth +
          size_t(reg_hidden - 1) * (2 * kHeadWidth * kHeadWidth + kHeadWidth) + kHeadWidth + 1;
 }
@@ -43,16 +43,18 @@ struct FusedArgs {
   const int32_t* perm;        // sorted slot -> caller index
   const int64_t* offsets;     // [n+1], rows in sorted order
   const int32_t* idx;         // neighbour entries, caller indices
-  const double* enc;          // packed encoder tables
-  const double* head;         // packed head tables
-  const double* qc;           // [16][20] angular coefficients
+  // network tables and workspace hold the kernel's arithmetic type
+  // (float64 or float32, mlip_hparams.precision)
+  const void* enc;            // packed encoder tables
+  const void* head;           // packed head tables
+  const void* qc;             // [16][20] angular coefficients
   double* energy;             // [n] or null
   double* forces;             // [n][3], zeroed before launch
   double* virial;             // [n][9] or null
   double* totals;             // [10]: E, W (zeroed before launch)
   unsigned long long* counters;  // [0] active pairs (zeroed before launch)
-  double* ws;                 // per-block workspace
-  long long ws_slot;          // doubles per block slot
+  void* ws;                   // per-block workspace
+  long long ws_slot;          // values per block slot
   double box[3];
   double inv_box[3];
   double rc, rc2;
@@ -85,14 +87,15 @@ struct mlip_ctx {
   std::string err;
   size_t bytes = 0;
 
-  // weights and tables
-  double* d_enc = nullptr;
-  size_t enc_stride = 0;
+  // weights and tables, in the kernel's arithmetic type (elem_bytes each)
+  size_t elem_bytes = 8;
+  unsigned char* d_enc = nullptr;
+  size_t enc_stride = 0;      // values per encoder table
   int n_enc = 0;
-  double* d_head = nullptr;
-  size_t head_stride = 0;
+  unsigned char* d_head = nullptr;
+  size_t head_stride = 0;     // values per head table
   int n_head = 0;
-  double* d_qc = nullptr;
+  unsigned char* d_qc = nullptr;
   double* d_inv_mass = nullptr;   // per species, acceleration factor / mass
   bool masses_set = false;
 
@@ -121,8 +124,9 @@ struct mlip_ctx {
   int64_t n_builds = 0;
 
   // fused kernel
-  double* d_ws = nullptr;
+  unsigned char* d_ws = nullptr;  // workspace, cap_ws bytes
   size_t cap_ws = 0;
+  size_t ws_slot = 0;             // values per work-group slot
   double* d_totals = nullptr;               // [16]
   unsigned long long* d_counters = nullptr; // [4]
   int32_t* d_flags = nullptr;               // [4]
@@ -158,8 +162,8 @@ hipError_t launch_fill_i32(int32_t* p, int64_t n, int32_t v, hipStream_t s);
 hipError_t launch_fill_f64(double* p, int64_t n, double v, hipStream_t s);
 hipError_t launch_fill_u64(unsigned long long* p, int64_t n, hipStream_t s);
 
-// fused.hip
-hipError_t launch_fused(int k, const FusedArgs& a, int n_blocks, hipStream_t s);
+// fused.hip (precision 64 or 32)
+hipError_t launch_fused(int k, int precision, const FusedArgs& a, int n_blocks, hipStream_t s);
 
 // md.hip
 hipError_t launch_md_first_half(double* pos, double* vel, const double* forces, const int32_t* types,

@@ -1,0 +1,133 @@
+"""GPU parity of the float32 network path (mlip_hparams.precision = 32)
+against the float64 oracle on identical seeded inputs.
+
+The bar is relative: for each output array (E_i, F, per-atom virial) the
+largest absolute deviation from the oracle must stay within 1e-4 of that
+array's largest oracle magnitude.  Neighbour sets do not depend on the
+network precision and must be identical."""
+import dataclasses
+
+import numpy as np
+import pytest
+
+import synth
+import oracle
+from oracle.model import Model, evaluate
+from oracle.neighbors import neighbor_list
+from tests.gpu_helpers import gpu_eval, assert_same_neighbor_sets, max_abs, log, oracle_sample, to_dev
+
+pytestmark = pytest.mark.gpu
+
+REL_TOL = 1e-4
+
+
+def rel_err(a, ref):
+    scale = float(np.max(np.abs(ref)))
+    return max_abs(a, ref) / scale if scale > 0 else max_abs(a, ref)
+
+
+def _hp32(hp):
+    return dataclasses.replace(hp, precision=32)
+
+
+def _compare(hp, weights, pos, types, box, label):
+    hp = _hp32(hp)
+    log(f"[fp32] {label}: N={len(pos)}")
+    g = gpu_eval(hp, weights, pos, types, box)
+    m = Model(hp, weights)
+    off, idx = neighbor_list(pos, box, m.rc + m.skin)
+    goff, gidx = g["pot"].neighbors()
+    assert_same_neighbor_sets(goff, gidx, off, idx)
+    ref = evaluate(m, pos, types, box, off, idx)
+    eE, eF, eV = rel_err(g["E_i"], ref["E_i"]), rel_err(g["F"], ref["F"]), rel_err(g["virial"], ref["virial"])
+    log(f"[fp32] {label}: rel dE={eE:.2e} dF={eF:.2e} dW={eV:.2e}")
+    assert eE <= REL_TOL, eE
+    assert eF <= REL_TOL, eF
+    assert eV <= REL_TOL, eV
+    assert abs(g["totals"][0] - ref["E"]) <= REL_TOL * abs(ref["E"]) + REL_TOL * len(pos)
+    st = g["stats"]
+    assert st["n_active_pairs"] == len(oracle.neighbors.active_rows(pos, box, off, idx, m.rc)[0])
+    g["pot"].close()
+    return g, ref
+
+
+VARIANTS = {
+    "default": {},
+    "lmax0": {"lmax": 0},
+    "lmax2": {"lmax": 2},
+    "enc_universal": {"enc_cond": 0},
+    "head_universal": {"reg_cond": 0},
+    "enc_hidden1": {"enc_hidden": 1},
+    "deep": {"enc_hidden": 5, "reg_hidden": 6},
+}
+
+
+@pytest.mark.parametrize("variant", list(VARIANTS))
+def test_fp32_binary_fcc_variants(variant):
+    w = synth.make_workload("fcc-binary-4", seed=3, hp_overrides=VARIANTS[variant])
+    _compare(w.hp, w.weights, w.pos, w.types, w.box, f"fcc-binary-4/{variant}")
+
+
+@pytest.mark.parametrize("name,n", [("fcc-ternary-64", 4), ("fcc-hea6-128", 5), ("bcc-unary-32", 6)])
+def test_fp32_preset_shapes(name, n):
+    w = synth.make_workload(name, seed=5, n=n)
+    _compare(w.hp, w.weights, w.pos, w.types, w.box, f"{name}/n={n}")
+
+
+def test_fp32_ragged_and_sparse():
+    rng = np.random.default_rng(21)
+    w = synth.make_workload("fcc-hea6-128", seed=11, n=4)
+    perm = rng.permutation(len(w.pos))
+    pos = w.pos[perm] + w.box * rng.integers(-1, 2, (len(w.pos), 3))
+    types = w.types[perm].copy()
+    types[:29] = 2
+    _compare(w.hp, w.weights, pos, types, w.box, "ragged")
+    box = np.array([40.0, 41.0, 43.0])
+    cl = synth.random_cluster(rng, 30, 3, 6.0, min_dist=2.0) + 20.0
+    iso = np.array([[2.0, 2.0, 2.0], [35.0, 4.0, 30.0]])
+    pos = np.concatenate([cl, iso])
+    types = rng.integers(0, 3, len(pos)).astype(np.int32)
+    hp = synth.HParams(n_species=3)
+    g, _ = _compare(hp, synth.random_weights(hp, 8), pos, types, box, "sparse")
+
+
+def test_fp32_agrees_with_fp64_path():
+    """Both instantiations on the same input: the float32 path deviates from
+    the float64 path by no more than from the oracle's bar."""
+    w = synth.make_workload("fcc-hea6-128", seed=2, n=6)
+    g64 = gpu_eval(w.hp, w.weights, w.pos, w.types, w.box)
+    g32 = gpu_eval(_hp32(w.hp), w.weights, w.pos, w.types, w.box)
+    for key in ("E_i", "F", "virial"):
+        e = rel_err(g32[key], g64[key])
+        log(f"[fp32] vs float64 path {key}: rel {e:.2e}")
+        assert e <= REL_TOL
+    g64["pot"].close()
+    g32["pot"].close()
+
+
+def test_fp32_full_size_sampled():
+    """8,388,608-atom 6-component FCC in the launch configuration of the
+    benchmark, float32 network: sampled atoms against the oracle."""
+    import torch
+    from paper_2608_16329_amd import Potential
+    w = synth.make_workload("fcc-hea6-128", seed=0, hp_overrides={"precision": 32})
+    N = len(w.pos)
+    log(f"[fp32] full size N={N}")
+    pot = Potential(w.hp, w.weights)
+    p = to_dev(w.pos)
+    t = to_dev(w.types)
+    pot.build_neighbors(p, t, w.box)
+    F = torch.empty((N, 3), dtype=torch.float64, device="cuda:0")
+    E = torch.empty(N, dtype=torch.float64, device="cuda:0")
+    V = torch.empty((N, 9), dtype=torch.float64, device="cuda:0")
+    pot.compute(p, F, E, V)
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(12)
+    atoms = rng.choice(N, 48, replace=False)
+    m = Model(w.hp, w.weights)
+    Er, Fr, Vr = oracle_sample(m, w.pos, w.types, w.box, atoms)
+    Eg, Fg, Vg = E.cpu().numpy()[atoms], F.cpu().numpy()[atoms], V.cpu().numpy()[atoms]
+    eE, eF, eV = rel_err(Eg, Er), rel_err(Fg, Fr), rel_err(Vg, Vr)
+    log(f"[fp32] full size sampled: rel dE={eE:.2e} dF={eF:.2e} dW={eV:.2e}")
+    assert eE <= REL_TOL and eF <= REL_TOL and eV <= REL_TOL
+    pot.close()

@@ -56,7 +56,7 @@ def test_invalid_hparams(binding):
 
 
 @pytest.mark.parametrize("over", [{"k": 24}, {"lmax": 4}, {"angular": 1}, {"enc_width": 64},
-                                  {"reg_width": 32}, {"precision": 32}, {"n_species": 17}, {"enc_hidden": 9}])
+                                  {"reg_width": 32}, {"precision": 16}, {"n_species": 17}, {"enc_hidden": 9}])
 def test_create_rejects_unsupported_before_device(binding, over):
     hp = synth.HParams(n_species=2)
     for k, v in over.items():
