@@ -173,7 +173,7 @@ __device__ __forceinline__ void monomial_grads(R x, R y, R z, R gx[kMonomials], 
   gx[19] = 0; gy[19] = 0; gz[19] = 3 * zz;
 }
 
-template <int K, int TM, typename R>
+template <int K, int TM, typename R, int NW>
 struct Smem {
   R P[TM][kAngRows][K + 1];  // moment, then its adjoint W (padded rows)
   R xT[4 * K][16];           // head input vec(G), feature-major
@@ -192,7 +192,7 @@ struct Smem {
   R l0[kMaxSpecies][2][kEncWidth];  // w0, b0 of the tile's encoder tables, by neighbour species
   int pair_j[kEntCap];
   unsigned char pair_a[kEntCap];
-  int wsum[kWaves];
+  int wsum[NW];
   int a0;
   int ch_start[kChunkCap];
   unsigned char ch_count[kChunkCap];
@@ -209,8 +209,8 @@ struct PairPos {
   double x, y, z;
 };
 
-template <int K, int TM, typename R>
-__device__ __forceinline__ PairPos load_pair_pos(const FusedArgs& A, const Smem<K, TM, R>& S, int ch) {
+template <int K, int TM, typename R, int NW>
+__device__ __forceinline__ PairPos load_pair_pos(const FusedArgs& A, const Smem<K, TM, R, NW>& S, int ch) {
   const int c = threadIdx.x & 15;
   PairPos p{0.0, 0.0, 0.0};
   if (c < S.ch_count[ch]) {
@@ -224,8 +224,8 @@ __device__ __forceinline__ PairPos load_pair_pos(const FusedArgs& A, const Smem<
 
 // Pass 1 on one chunk: encoder forward + tangent, moment accumulation and
 // the workspace write of (m, dm).
-template <int K, int TM, typename R>
-__device__ void pass1_chunk(const FusedArgs& A, Smem<K, TM, R>& S, int ch, const PairPos pp, R* __restrict__ wsc) {
+template <int K, int TM, typename R, int NW>
+__device__ void pass1_chunk(const FusedArgs& A, Smem<K, TM, R, NW>& S, int ch, const PairPos pp, R* __restrict__ wsc) {
   constexpr int KT = K / 16;
   const int lane = threadIdx.x & 63, g = lane >> 4, c = lane & 15;
   const int start = S.ch_start[ch], count = S.ch_count[ch];
@@ -256,8 +256,10 @@ __device__ void pass1_chunk(const FusedArgs& A, Smem<K, TM, R>& S, int ch, const
   constexpr int NH = 8 / VW;                // loads per hidden-layer k-step
   constexpr int VO = KT < VW ? KT : VW;     // fragments per output-layer load
   constexpr int NO = KT / VO;               // loads per output-layer k-step
-  constexpr int kRing = sizeof(R) == 8 ? 3 : 4;
-  constexpr int kRingOut = sizeof(R) == 8 ? 3 : 6;
+  // ring depths: with two wavefronts per SIMD (NW = 8) the other wavefront
+  // covers part of the latency and registers are scarcer
+  constexpr int kRing = (sizeof(R) == 8 || NW == 8) ? 3 : 4;
+  constexpr int kRingOut = (sizeof(R) == 8 || NW == 8) ? 3 : 6;
   typedef R vh_t __attribute__((ext_vector_type(VW)));
   typedef R vo_t __attribute__((ext_vector_type(VO)));
   vh_t wb[kRing][NH];
@@ -276,9 +278,10 @@ __device__ void pass1_chunk(const FusedArgs& A, Smem<K, TM, R>& S, int ch, const
 #pragma unroll
       for (int u = 0; u < NO; ++u) wo[p][u] = f[(p * NO + u) * 64];
   };
-  // float32 issues each product's first fragments before the activation
-  // work in front of it; float64 has no registers to spare for that
-  constexpr bool kEarly = sizeof(R) == 4;
+  // float32 with one wavefront per SIMD issues each product's first
+  // fragments before the activation work in front of it; the other
+  // configurations have no registers to spare for that
+  constexpr bool kEarly = sizeof(R) == 4 && NW == 4;
   const R* __restrict__ layer = tab + 2 * kEncWidth;
   if (kEarly) {
     if (A.enc_hidden > 1)
@@ -444,8 +447,8 @@ struct Pass2In {
   PairPos pp;
 };
 
-template <int K, int TM, typename R>
-__device__ __forceinline__ void pass2_load(const FusedArgs& A, const Smem<K, TM, R>& S, int ch,
+template <int K, int TM, typename R, int NW>
+__device__ __forceinline__ void pass2_load(const FusedArgs& A, const Smem<K, TM, R, NW>& S, int ch,
                                            const R* __restrict__ wsc, Pass2In<K, R>& in) {
   constexpr int VW = 16 / int(sizeof(R));
   constexpr int NV = K / 4 / VW;  // 16-byte loads per lane for m (and for dm)
@@ -470,8 +473,8 @@ __device__ __forceinline__ void pass2_load(const FusedArgs& A, const Smem<K, TM,
 }
 
 // Pass 2 on one chunk: W contractions, partial forces and scatter.
-template <int K, int TM, typename R>
-__device__ void pass2_chunk(const FusedArgs& A, Smem<K, TM, R>& S, int ch, const Pass2In<K, R>& in) {
+template <int K, int TM, typename R, int NW>
+__device__ void pass2_chunk(const FusedArgs& A, Smem<K, TM, R, NW>& S, int ch, const Pass2In<K, R>& in) {
   constexpr int KT = K / 16;
   const int lane = threadIdx.x & 63, g = lane >> 4, c = lane & 15;
   const int start = S.ch_start[ch], count = S.ch_count[ch];
@@ -576,19 +579,19 @@ __device__ void pass2_chunk(const FusedArgs& A, Smem<K, TM, R>& S, int ch, const
 
 // Descriptor (Eq. 5), head forward and backward (Eq. 6) and W = dE/dP
 // (Eq. 7) for the tile on MFMA: the tile's atoms are the 16 columns of every
-// product and wavefront w owns rows 16w..16w+15 of each 64-wide layer.
+// product and wavefront w < 4 owns rows 16w..16w+15 of each 64-wide layer.
 // Activations live in LDS feature-major ([feature][atom]) so that B-operand
 // reads are contiguous; pre-activations stay in registers for the backward
 // pass.
-template <int K, int TM, typename R>
-__device__ void head_stage(const FusedArgs& A, Smem<K, TM, R>& S) {
+template <int K, int TM, typename R, int NW>
+__device__ void head_stage(const FusedArgs& A, Smem<K, TM, R, NW>& S) {
   constexpr int RW = kHeadWidth;
   constexpr int HS = 2 * RW * RW + RW;  // one hidden layer: A_t and A_t^T fragments, c_t
   const int tid = threadIdx.x, lane = tid & 63, g = lane >> 4, c = lane & 15, w = tid >> 6;
   const int na = S.na;
   const int nin = (A.lmax + 1) * K;
   const int tin = nin / 16;
-  for (int u = tid; u < 16 * nin; u += kThreads) {
+  for (int u = tid; u < 16 * nin; u += (64 * NW)) {
     const int a = u & 15, in = u >> 4;
     R v = 0;
     if (a < na) {
@@ -609,15 +612,20 @@ __device__ void head_stage(const FusedArgs& A, Smem<K, TM, R>& S) {
   const R* __restrict__ c0 = A0Tf + RW * nin;
   const R* __restrict__ hid = c0 + RW;
   const R* __restrict__ aout = hid + (A.reg_hidden - 1) * HS;
-  // this lane's result rows are 16 w + drow(q, g)
+  // this lane's result rows are 16 w + drow(q, g); with more than 4
+  // wavefronts the others only join the barriers of the row-parallel steps
+  const bool rw = w < RW / 16;
 #define ROW(q) (16 * w + drow<R>(q, g))
 
   // layer 0: z0 = A0 x + c0
-  v4<R> z0 = v4<R>{c0[ROW(0)], c0[ROW(1)], c0[ROW(2)], c0[ROW(3)]};
-  for (int ks = 0; ks < nin / 4; ++ks)
-    z0 = mfma(A0f[(ks * 4 + w) * 64 + lane], S.xT[16 * (ks >> 2) + drow<R>(ks & 3, g)][c], z0);
+  v4<R> z0 = v4<R>{0, 0, 0, 0};
+  if (rw) {
+    z0 = v4<R>{c0[ROW(0)], c0[ROW(1)], c0[ROW(2)], c0[ROW(3)]};
+    for (int ks = 0; ks < nin / 4; ++ks)
+      z0 = mfma(A0f[(ks * 4 + w) * 64 + lane], S.xT[16 * (ks >> 2) + drow<R>(ks & 3, g)][c], z0);
 #pragma unroll
-  for (int q = 0; q < 4; ++q) S.yT[ROW(q)][c] = z0[q] * sigmoid(z0[q]);
+    for (int q = 0; q < 4; ++q) S.yT[ROW(q)][c] = z0[q] * sigmoid(z0[q]);
+  }
   __syncthreads();
 
   // residual layers: y <- y + silu(A_t y + c_t)
@@ -627,14 +635,19 @@ __device__ void head_stage(const FusedArgs& A, Smem<K, TM, R>& S) {
     if (t >= A.reg_hidden) break;
     const R* __restrict__ Af = hid + (t - 1) * HS;
     const R* __restrict__ ct = Af + 2 * RW * RW;
-    v4<R> z = v4<R>{ct[ROW(0)], ct[ROW(1)], ct[ROW(2)], ct[ROW(3)]};
+    v4<R> z = v4<R>{0, 0, 0, 0};
+    if (rw) {
+      z = v4<R>{ct[ROW(0)], ct[ROW(1)], ct[ROW(2)], ct[ROW(3)]};
 #pragma unroll
-    for (int ks = 0; ks < 16; ++ks)
-      z = mfma(Af[(ks * 4 + w) * 64 + lane], S.yT[16 * (ks >> 2) + drow<R>(ks & 3, g)][c], z);
+      for (int ks = 0; ks < 16; ++ks)
+        z = mfma(Af[(ks * 4 + w) * 64 + lane], S.yT[16 * (ks >> 2) + drow<R>(ks & 3, g)][c], z);
+    }
     zeta[t] = z;
     __syncthreads();
+    if (rw) {
 #pragma unroll
-    for (int q = 0; q < 4; ++q) S.yT[ROW(q)][c] += z[q] * sigmoid(z[q]);
+      for (int q = 0; q < 4; ++q) S.yT[ROW(q)][c] += z[q] * sigmoid(z[q]);
+    }
     __syncthreads();
   }
   if (tid < na) {
@@ -644,32 +657,38 @@ __device__ void head_stage(const FusedArgs& A, Smem<K, TM, R>& S) {
   }
 
   // backward: d <- d + A_t^T (silu'(zeta_t) d), starting from d = a_out
-  v4<R> d = v4<R>{aout[ROW(0)], aout[ROW(1)], aout[ROW(2)], aout[ROW(3)]};
+  v4<R> d = rw ? v4<R>{aout[ROW(0)], aout[ROW(1)], aout[ROW(2)], aout[ROW(3)]} : v4<R>{0, 0, 0, 0};
 #pragma unroll
   for (int t = kMaxHidden - 1; t >= 1; --t) {
     if (t >= A.reg_hidden) continue;
     const R* __restrict__ ATf = hid + (t - 1) * HS + RW * RW;
+    if (rw) {
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const R z = zeta[t][q], sg = sigmoid(z);
-      S.gT[ROW(q)][c] = sg * (R(1) + z * (R(1) - sg)) * d[q];
+      for (int q = 0; q < 4; ++q) {
+        const R z = zeta[t][q], sg = sigmoid(z);
+        S.gT[ROW(q)][c] = sg * (R(1) + z * (R(1) - sg)) * d[q];
+      }
     }
     __syncthreads();
-    v4<R> acc = v4<R>{0, 0, 0, 0};
+    if (rw) {
+      v4<R> acc = v4<R>{0, 0, 0, 0};
 #pragma unroll
-    for (int ks = 0; ks < 16; ++ks)
-      acc = mfma(ATf[(ks * 4 + w) * 64 + lane], S.gT[16 * (ks >> 2) + drow<R>(ks & 3, g)][c], acc);
-    d += acc;
+      for (int ks = 0; ks < 16; ++ks)
+        acc = mfma(ATf[(ks * 4 + w) * 64 + lane], S.gT[16 * (ks >> 2) + drow<R>(ks & 3, g)][c], acc);
+      d += acc;
+    }
     __syncthreads();
   }
+  if (rw) {
 #pragma unroll
-  for (int q = 0; q < 4; ++q) {
-    const R z = z0[q], sg = sigmoid(z);
-    S.gT[ROW(q)][c] = sg * (R(1) + z * (R(1) - sg)) * d[q];
+    for (int q = 0; q < 4; ++q) {
+      const R z = z0[q], sg = sigmoid(z);
+      S.gT[ROW(q)][c] = sg * (R(1) + z * (R(1) - sg)) * d[q];
+    }
   }
   __syncthreads();
   // dE/dx = A0^T g0, then W[0][col] = dE/dG[0][col], W[m][col] = 2 dE/dG[l][col] P[m][col]
-  for (int tt = w; tt < tin; tt += kWaves) {
+  for (int tt = w; tt < tin; tt += NW) {
     v4<R> acc = v4<R>{0, 0, 0, 0};
 #pragma unroll
     for (int ks = 0; ks < 16; ++ks)
@@ -691,17 +710,17 @@ __device__ void head_stage(const FusedArgs& A, Smem<K, TM, R>& S) {
 #undef ROW
 }
 
-template <int K, int TM, typename R>
-__global__ __launch_bounds__(kThreads, 1) void k_fused(FusedArgs A) {
+template <int K, int TM, typename R, int NW>
+__global__ __launch_bounds__(64 * NW, 1) void k_fused(FusedArgs A) {
   extern __shared__ __align__(16) unsigned char smem_raw[];
-  Smem<K, TM, R>& S = *reinterpret_cast<Smem<K, TM, R>*>(smem_raw);
+  Smem<K, TM, R, NW>& S = *reinterpret_cast<Smem<K, TM, R, NW>*>(smem_raw);
   const int tid = threadIdx.x, wave = tid >> 6;
   const long long chunk_elems = 2LL * K * 16;
   R* __restrict__ ws_slot = static_cast<R*>(A.ws) + (long long)blockIdx.x * A.ws_slot;
   const R* __restrict__ enc = static_cast<const R*>(A.enc);
   const R* __restrict__ qc = static_cast<const R*>(A.qc);
 
-  for (int u = tid; u < kAngRows * kMonomials; u += kThreads) S.qc[u / kMonomials][u % kMonomials] = qc[u];
+  for (int u = tid; u < kAngRows * kMonomials; u += (64 * NW)) S.qc[u / kMonomials][u % kMonomials] = qc[u];
 
   // XCD-aware assignment: blocks are dispatched round-robin over the 8 XCDs,
   // so block b works on the b%8-th contiguous eighth of the tile list and
@@ -729,7 +748,7 @@ __global__ __launch_bounds__(kThreads, 1) void k_fused(FusedArgs A) {
     __syncthreads();
     const int na = S.na;
     const int a0 = S.a0;
-    for (int u = tid; u < A.C * 2 * kEncWidth; u += kThreads) {
+    for (int u = tid; u < A.C * 2 * kEncWidth; u += (64 * NW)) {
       const int sj = u / (2 * kEncWidth), rem = u % (2 * kEncWidth);
       const int si = S.tile_species;
       const int tau = A.enc_cond == 2 ? si * A.C + sj : (A.enc_cond == 1 ? sj : 0);
@@ -754,12 +773,12 @@ __global__ __launch_bounds__(kThreads, 1) void k_fused(FusedArgs A) {
       for (int k = 0; k < 9; ++k) S.Wi[tid][k] = 0.0;
       S.Ei[tid] = 0.0;
     }
-    for (int u = tid; u < kMaxSpecies * TM; u += kThreads) S.cnt[u / TM][u % TM] = 0;
-    for (int u = tid; u < TM * kAngRows * (K + 1); u += kThreads) (&S.P[0][0][0])[u] = R(0);
+    for (int u = tid; u < kMaxSpecies * TM; u += (64 * NW)) S.cnt[u / TM][u % TM] = 0;
+    for (int u = tid; u < TM * kAngRows * (K + 1); u += (64 * NW)) (&S.P[0][0][0])[u] = R(0);
     __syncthreads();
     const int nent = S.ent_base[na];
     const long long ebase = S.row_beg[0];
-    constexpr int kPer = kEntCap / kThreads;
+    constexpr int kPer = kEntCap / (64 * NW);
     int ej[kPer], ea[kPer], es[kPer];
     int my_active = 0;
     {
@@ -852,25 +871,25 @@ __global__ __launch_bounds__(kThreads, 1) void k_fused(FusedArgs A) {
     const int nch = S.n_chunks;
     {
       PairPos next = wave < nch ? load_pair_pos(A, S, wave) : PairPos{0.0, 0.0, 0.0};
-      for (int ch = wave; ch < nch; ch += kWaves) {
+      for (int ch = wave; ch < nch; ch += NW) {
         const PairPos cur = next;
-        if (ch + kWaves < nch) next = load_pair_pos(A, S, ch + kWaves);
-        pass1_chunk<K, TM, R>(A, S, ch, cur, ws_slot + ch * chunk_elems);
+        if (ch + NW < nch) next = load_pair_pos(A, S, ch + NW);
+        pass1_chunk<K, TM, R, NW>(A, S, ch, cur, ws_slot + ch * chunk_elems);
       }
     }
     __syncthreads();
 
     // ---- C: descriptor, head, W ------------------------------------------
-    head_stage<K, TM, R>(A, S);
+    head_stage<K, TM, R, NW>(A, S);
 
     // ---- D: pass 2 ---------------------------------------------------------
     {
       Pass2In<K, R> next;
       if (wave < nch) pass2_load(A, S, wave, ws_slot + wave * chunk_elems, next);
-      for (int ch = wave; ch < nch; ch += kWaves) {
+      for (int ch = wave; ch < nch; ch += NW) {
         const Pass2In<K, R> cur = next;
-        if (ch + kWaves < nch) pass2_load(A, S, ch + kWaves, ws_slot + (ch + kWaves) * chunk_elems, next);
-        pass2_chunk<K, TM, R>(A, S, ch, cur);
+        if (ch + NW < nch) pass2_load(A, S, ch + NW, ws_slot + (ch + NW) * chunk_elems, next);
+        pass2_chunk<K, TM, R, NW>(A, S, ch, cur);
       }
     }
     __syncthreads();
@@ -910,25 +929,25 @@ __global__ __launch_bounds__(kThreads, 1) void k_fused(FusedArgs A) {
   }
 }
 
-template <int K, int TM, typename R>
+template <int K, int TM, typename R, int NW>
 hipError_t launch_k(const FusedArgs& a, int n_blocks, hipStream_t s) {
-  const size_t smem = sizeof(Smem<K, TM, R>);
+  const size_t smem = sizeof(Smem<K, TM, R, NW>);
   static bool attr_set = false;
   if (!attr_set) {
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_fused<K, TM, R>),
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_fused<K, TM, R, NW>),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, int(smem));
     if (e != hipSuccess) return e;
     attr_set = true;
   }
-  k_fused<K, TM, R><<<dim3(unsigned(n_blocks)), dim3(kThreads), smem, s>>>(a);
+  k_fused<K, TM, R, NW><<<dim3(unsigned(n_blocks)), dim3(64 * NW), smem, s>>>(a);
   return hipGetLastError();
 }
 
 }  // namespace
 
 hipError_t launch_fused(int k, int precision, const FusedArgs& a, int n_blocks, hipStream_t s) {
-  if (k == 32 && precision == 64) return launch_k<32, kTileMax, double>(a, n_blocks, s);
-  if (k == 32 && precision == 32) return launch_k<32, kTileMax, float>(a, n_blocks, s);
+  if (k == 32 && precision == 64) return launch_k<32, kTileMax, double, 4>(a, n_blocks, s);
+  if (k == 32 && precision == 32) return launch_k<32, kTileMax, float, 8>(a, n_blocks, s);
   return hipErrorInvalidValue;
 }
 
