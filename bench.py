@@ -294,6 +294,8 @@ def main() -> int:
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--precision", type=int, choices=(64, 32), default=64,
                     help="network arithmetic: 64 (float64) or 32 (float32 network, float64 geometry and sums)")
+    ap.add_argument("--hp", default="",
+                    help="comma-separated hyper-parameter overrides, e.g. k=64,lmax=2,enc_cond=1")
     ap.add_argument("--rebuild-every", type=int, default=10)
     ap.add_argument("--cpu-sample", type=int, default=100000, help="oracle sample size (atoms); 0 disables")
     ap.add_argument("--calibrate-copy-bytes", type=int, default=0,
@@ -325,8 +327,11 @@ def main() -> int:
     from paper_2608_16329_amd import Potential
 
     t_gen = time.perf_counter()
-    w = synth.make_workload(args.workload, seed=args.seed, n=args.cells,
-                            hp_overrides={"precision": args.precision})
+    overrides = {"precision": args.precision}
+    for item in filter(None, args.hp.split(",")):
+        key, val = item.split("=")
+        overrides[key.strip()] = int(val)
+    w = synth.make_workload(args.workload, seed=args.seed, n=args.cells, hp_overrides=overrides)
     N = len(w.pos)
     log(f"[bench] workload {w.description}: N={N} generated in {time.perf_counter() - t_gen:.1f}s")
     dev = torch.device("cuda:0")
@@ -427,7 +432,9 @@ def main() -> int:
                    "rebuild_every": args.rebuild_every, "rebuilds_in_timed_steps": rebuilds,
                    "active_pairs_per_atom": float(np.mean(active_pairs)) / N,
                    "listed_pairs_per_atom": st["n_listed_pairs"] / N, "tile_atoms": st["tile_atoms"],
-                   "blocks": st["n_blocks"], "seed": args.seed, "precision": args.precision},
+                   "blocks": st["n_blocks"], "seed": args.seed, "precision": args.precision,
+                   "enc_cond": w.hp.enc_cond, "reg_cond": w.hp.reg_cond, "enc_hidden": w.hp.enc_hidden,
+                   "reg_hidden": w.hp.reg_hidden},
         "roofline": {"bound": "mfma", "achieved": achieved, "peak": PEAK_TFLOPS[args.precision], "unit": "TFLOP/s",
                      "frac": achieved / PEAK_TFLOPS[args.precision],
                      "traffic": measured_traffic(w.description, N, args.precision),

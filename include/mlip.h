@@ -69,7 +69,7 @@ typedef struct {
   int32_t n_species;   /* C >= 1 (the GPU path supports C <= 16)                  */
   double  cutoff;      /* r_c in A                                               */
   double  skin;        /* Verlet skin in A; neighbour lists use r_c + skin       */
-  int32_t k;           /* radial feature width (GPU path: 32)                    */
+  int32_t k;           /* radial feature width (GPU path: 16, 32 or 64)          */
   int32_t lmax;        /* maximum angular order (GPU path: 0..3)                 */
   int32_t angular;     /* 0 irreducible harmonic basis, d = (lmax+1)^2
                           (1 = Cartesian monomials; not on the GPU path)         */

@@ -77,7 +77,7 @@ bool gpu_supported(const mlip_hparams* hp, std::string* why) {
   if (hp->precision != 64 && hp->precision != 32) return *why = "precision must be 64 or 32", false;
   if (hp->angular != 0) return *why = "only the irreducible angular basis runs on the GPU path", false;
   if (hp->lmax < 0 || hp->lmax > 3) return *why = "lmax must be in 0..3 on the GPU path", false;
-  if (hp->k != 32) return *why = "k must be 32 on the GPU path", false;
+  if (hp->k != 16 && hp->k != 32 && hp->k != 64) return *why = "k must be 16, 32 or 64 on the GPU path", false;
   if (hp->enc_width != kEncWidth) return *why = "enc_width must be 128 on the GPU path", false;
   if (hp->reg_width != kHeadWidth) return *why = "reg_width must be 64 on the GPU path", false;
   if (hp->enc_hidden < 1 || hp->enc_hidden > kMaxHidden) return *why = "enc_hidden must be in 1..8", false;
@@ -344,7 +344,7 @@ mlip_status mlip_build_neighbors(mlip_ctx* ctx, int64_t n_atoms, const double* p
   ctx->max_row = flags[1];
 
   // fused-kernel tiling and workspace
-  const int T = std::max(1, std::min(kTileMax, kEntCap / std::max(1, ctx->max_row)));
+  const int T = std::max(1, std::min(fused_tile_max(ctx->hp.k, ctx->hp.precision), kEntCap / std::max(1, ctx->max_row)));
   ctx->tile_atoms = T;
   int64_t tiles = 0;
   for (int sp_i = 0; sp_i < C; ++sp_i) tiles += (int64_t(sp[sp_i + 1] - sp[sp_i]) + T - 1) / T;

@@ -176,9 +176,16 @@ __device__ __forceinline__ void monomial_grads(R x, R y, R z, R gx[kMonomials], 
 template <int K, int TM, typename R, int NW>
 struct Smem {
   R P[TM][kAngRows][K + 1];  // moment, then its adjoint W (padded rows)
-  R xT[4 * K][16];           // head input vec(G), feature-major
-  R yT[kHeadWidth][16];      // head activations
-  R gT[kHeadWidth][16];      // head backward scratch
+  // Pass 1 reads the first-layer weights; the head runs after pass 1 and
+  // before the next tile is staged, so its activations reuse those bytes.
+  union {
+    R l0[kMaxSpecies][2][kEncWidth];  // w0, b0 of the tile's encoder tables, by neighbour species
+    struct {
+      R xT[4 * K][16];              // head input vec(G), feature-major
+      R yT[kHeadWidth][16];         // head activations
+      R gT[kHeadWidth][16];         // head backward scratch
+    } hd;
+  } u;
   R qc[kAngRows][kMonomials];
   double tpos[TM][3];
   double Fi[TM][3];
@@ -189,7 +196,6 @@ struct Smem {
   int orig[TM];
   int cnt[kMaxSpecies][TM];
   int base[kMaxSpecies][TM];
-  R l0[kMaxSpecies][2][kEncWidth];  // w0, b0 of the tile's encoder tables, by neighbour species
   int pair_j[kEntCap];
   unsigned char pair_a[kEntCap];
   int wsum[NW];
@@ -297,7 +303,7 @@ __device__ void pass1_chunk(const FusedArgs& A, Smem<K, TM, R, NW>& S, int ch, c
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int in = 16 * T + drow<R>(i, g);
-      const R w0 = S.l0[sj][0][in], z = w0 * r + S.l0[sj][1][in];
+      const R w0 = S.u.l0[sj][0][in], z = w0 * r + S.u.l0[sj][1][in];
       const R s = sigmoid(z);
       h[T][i] = z * s;
       dh[T][i] = s * (R(1) + z * (R(1) - s)) * w0;
@@ -602,7 +608,7 @@ __device__ void head_stage(const FusedArgs& A, Smem<K, TM, R, NW>& S) {
         for (int mm = l * l; mm < (l + 1) * (l + 1); ++mm) v += S.P[a][mm][col] * S.P[a][mm][col];
       }
     }
-    S.xT[in][a] = v;
+    S.u.hd.xT[in][a] = v;
   }
   __syncthreads();
 
@@ -622,9 +628,9 @@ __device__ void head_stage(const FusedArgs& A, Smem<K, TM, R, NW>& S) {
   if (rw) {
     z0 = v4<R>{c0[ROW(0)], c0[ROW(1)], c0[ROW(2)], c0[ROW(3)]};
     for (int ks = 0; ks < nin / 4; ++ks)
-      z0 = mfma(A0f[(ks * 4 + w) * 64 + lane], S.xT[16 * (ks >> 2) + drow<R>(ks & 3, g)][c], z0);
+      z0 = mfma(A0f[(ks * 4 + w) * 64 + lane], S.u.hd.xT[16 * (ks >> 2) + drow<R>(ks & 3, g)][c], z0);
 #pragma unroll
-    for (int q = 0; q < 4; ++q) S.yT[ROW(q)][c] = z0[q] * sigmoid(z0[q]);
+    for (int q = 0; q < 4; ++q) S.u.hd.yT[ROW(q)][c] = z0[q] * sigmoid(z0[q]);
   }
   __syncthreads();
 
@@ -640,19 +646,19 @@ __device__ void head_stage(const FusedArgs& A, Smem<K, TM, R, NW>& S) {
       z = v4<R>{ct[ROW(0)], ct[ROW(1)], ct[ROW(2)], ct[ROW(3)]};
 #pragma unroll
       for (int ks = 0; ks < 16; ++ks)
-        z = mfma(Af[(ks * 4 + w) * 64 + lane], S.yT[16 * (ks >> 2) + drow<R>(ks & 3, g)][c], z);
+        z = mfma(Af[(ks * 4 + w) * 64 + lane], S.u.hd.yT[16 * (ks >> 2) + drow<R>(ks & 3, g)][c], z);
     }
     zeta[t] = z;
     __syncthreads();
     if (rw) {
 #pragma unroll
-      for (int q = 0; q < 4; ++q) S.yT[ROW(q)][c] += z[q] * sigmoid(z[q]);
+      for (int q = 0; q < 4; ++q) S.u.hd.yT[ROW(q)][c] += z[q] * sigmoid(z[q]);
     }
     __syncthreads();
   }
   if (tid < na) {
     R e = aout[RW];
-    for (int o = 0; o < RW; ++o) e += aout[o] * S.yT[o][tid];
+    for (int o = 0; o < RW; ++o) e += aout[o] * S.u.hd.yT[o][tid];
     S.Ei[tid] = double(e);
   }
 
@@ -666,7 +672,7 @@ __device__ void head_stage(const FusedArgs& A, Smem<K, TM, R, NW>& S) {
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
         const R z = zeta[t][q], sg = sigmoid(z);
-        S.gT[ROW(q)][c] = sg * (R(1) + z * (R(1) - sg)) * d[q];
+        S.u.hd.gT[ROW(q)][c] = sg * (R(1) + z * (R(1) - sg)) * d[q];
       }
     }
     __syncthreads();
@@ -674,7 +680,7 @@ __device__ void head_stage(const FusedArgs& A, Smem<K, TM, R, NW>& S) {
       v4<R> acc = v4<R>{0, 0, 0, 0};
 #pragma unroll
       for (int ks = 0; ks < 16; ++ks)
-        acc = mfma(ATf[(ks * 4 + w) * 64 + lane], S.gT[16 * (ks >> 2) + drow<R>(ks & 3, g)][c], acc);
+        acc = mfma(ATf[(ks * 4 + w) * 64 + lane], S.u.hd.gT[16 * (ks >> 2) + drow<R>(ks & 3, g)][c], acc);
       d += acc;
     }
     __syncthreads();
@@ -683,7 +689,7 @@ __device__ void head_stage(const FusedArgs& A, Smem<K, TM, R, NW>& S) {
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       const R z = z0[q], sg = sigmoid(z);
-      S.gT[ROW(q)][c] = sg * (R(1) + z * (R(1) - sg)) * d[q];
+      S.u.hd.gT[ROW(q)][c] = sg * (R(1) + z * (R(1) - sg)) * d[q];
     }
   }
   __syncthreads();
@@ -692,7 +698,7 @@ __device__ void head_stage(const FusedArgs& A, Smem<K, TM, R, NW>& S) {
     v4<R> acc = v4<R>{0, 0, 0, 0};
 #pragma unroll
     for (int ks = 0; ks < 16; ++ks)
-      acc = mfma(A0Tf[(ks * tin + tt) * 64 + lane], S.gT[16 * (ks >> 2) + drow<R>(ks & 3, g)][c], acc);
+      acc = mfma(A0Tf[(ks * tin + tt) * 64 + lane], S.u.hd.gT[16 * (ks >> 2) + drow<R>(ks & 3, g)][c], acc);
     if (c < na) {
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
@@ -752,7 +758,7 @@ __global__ __launch_bounds__(64 * NW, 1) void k_fused(FusedArgs A) {
       const int sj = u / (2 * kEncWidth), rem = u % (2 * kEncWidth);
       const int si = S.tile_species;
       const int tau = A.enc_cond == 2 ? si * A.C + sj : (A.enc_cond == 1 ? sj : 0);
-      S.l0[sj][rem / kEncWidth][rem % kEncWidth] = enc[(long long)tau * A.enc_stride + rem];
+      S.u.l0[sj][rem / kEncWidth][rem % kEncWidth] = enc[(long long)tau * A.enc_stride + rem];
     }
     if (tid <= TM) {
       const int k = tid < na ? tid : na;
@@ -931,6 +937,7 @@ __global__ __launch_bounds__(64 * NW, 1) void k_fused(FusedArgs A) {
 
 template <int K, int TM, typename R, int NW>
 hipError_t launch_k(const FusedArgs& a, int n_blocks, hipStream_t s) {
+  static_assert(sizeof(Smem<K, TM, R, NW>) <= 160 * 1024, "tile state exceeds the 160 KB LDS of a CU");
   const size_t smem = sizeof(Smem<K, TM, R, NW>);
   static bool attr_set = false;
   if (!attr_set) {
@@ -945,9 +952,27 @@ hipError_t launch_k(const FusedArgs& a, int n_blocks, hipStream_t s) {
 
 }  // namespace
 
+// Instantiations: k in {16, 32, 64}; float64 with one wavefront per SIMD,
+// float32 with two; 16 atoms per tile except float64 at k = 64, whose moment
+// tiles need 8 to fit in LDS.
+int fused_tile_max(int k, int precision) { return (k == 64 && precision == 64) ? 8 : 16; }
+
 hipError_t launch_fused(int k, int precision, const FusedArgs& a, int n_blocks, hipStream_t s) {
-  if (k == 32 && precision == 64) return launch_k<32, kTileMax, double, 4>(a, n_blocks, s);
-  if (k == 32 && precision == 32) return launch_k<32, kTileMax, float, 8>(a, n_blocks, s);
+  if (precision == 64) {
+    switch (k) {
+      case 16: return launch_k<16, 16, double, 4>(a, n_blocks, s);
+      case 32: return launch_k<32, 16, double, 4>(a, n_blocks, s);
+      case 64: return launch_k<64, 8, double, 4>(a, n_blocks, s);
+      default: break;
+    }
+  } else if (precision == 32) {
+    switch (k) {
+      case 16: return launch_k<16, 16, float, 8>(a, n_blocks, s);
+      case 32: return launch_k<32, 16, float, 8>(a, n_blocks, s);
+      case 64: return launch_k<64, 16, float, 8>(a, n_blocks, s);
+      default: break;
+    }
+  }
   return hipErrorInvalidValue;
 }
 

@@ -15,7 +15,6 @@ namespace mlip {
 // Fused-kernel geometry (gfx950: 64-wide wavefronts, 160 KB LDS per CU).
 constexpr int kWaves = 4;                 // wavefronts per work-group (one per SIMD)
 constexpr int kThreads = kWaves * 64;     // work-group size
-constexpr int kTileMax = 16;              // centre atoms per tile (k = 16, 32)
 constexpr int kEntCap = 2048;             // listed neighbour entries per tile
 constexpr int kChunkCap = kEntCap / 16 + 16;
 constexpr int kMaxSpecies = 16;
@@ -60,7 +59,7 @@ struct FusedArgs {
   double rc, rc2;
   long long enc_stride, head_stride;
   int C, enc_cond, reg_cond, lmax, enc_hidden, reg_hidden;
-  int tile_atoms;             // atoms per tile (<= kTileMax)
+  int tile_atoms;             // atoms per tile (<= fused_tile_max)
   int n_tiles;
   int species_start[kMaxSpecies + 1];  // first sorted slot of each species
   int tile_start[kMaxSpecies + 1];     // first tile of each species
@@ -162,8 +161,9 @@ hipError_t launch_fill_i32(int32_t* p, int64_t n, int32_t v, hipStream_t s);
 hipError_t launch_fill_f64(double* p, int64_t n, double v, hipStream_t s);
 hipError_t launch_fill_u64(unsigned long long* p, int64_t n, hipStream_t s);
 
-// fused.hip (precision 64 or 32)
+// fused.hip (k 16, 32 or 64; precision 64 or 32)
 hipError_t launch_fused(int k, int precision, const FusedArgs& a, int n_blocks, hipStream_t s);
+int fused_tile_max(int k, int precision);  // centre atoms per tile of that instantiation
 
 // md.hip
 hipError_t launch_md_first_half(double* pos, double* vel, const double* forces, const int32_t* types,

@@ -59,6 +59,8 @@ VARIANTS = {
     "head_universal": {"reg_cond": 0},
     "enc_hidden1": {"enc_hidden": 1},
     "deep": {"enc_hidden": 5, "reg_hidden": 6},
+    "k16": {"k": 16},
+    "k64": {"k": 64},
 }
 
 

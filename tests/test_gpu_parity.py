@@ -54,6 +54,10 @@ VARIANTS = {
     "enc_hidden1": {"enc_hidden": 1},
     "enc_hidden2_reg2": {"enc_hidden": 2, "reg_hidden": 2},
     "deep": {"enc_hidden": 5, "reg_hidden": 6},
+    "k16": {"k": 16},
+    "k64": {"k": 64},
+    "k64_lmax1_universal": {"k": 64, "lmax": 1, "enc_cond": 0},
+    "k16_lmax0": {"k": 16, "lmax": 0},
 }
 
 
@@ -68,6 +72,13 @@ def test_binary_fcc_variants(variant):
 def test_preset_shapes(name, n):
     w = synth.make_workload(name, seed=5, n=n)
     _compare(w.hp, w.weights, w.pos, w.types, w.box, f"{name}/n={n}")
+
+
+@pytest.mark.parametrize("k", [16, 64])
+def test_k_sweep_six_species(k):
+    """Radial widths of the paper's k ablation on the 6-component FCC shape."""
+    w = synth.make_workload("fcc-hea6-128", seed=7, n=5, hp_overrides={"k": k})
+    _compare(w.hp, w.weights, w.pos, w.types, w.box, f"fcc-hea6-128/n=5/k={k}")
 
 
 def test_ragged_random_species_and_order():
