@@ -126,9 +126,13 @@ def summarize_traffic(fetch_dir: str, write_dir: str, bench_log: str, copy_bytes
                 f"{np.mean(wf):.4g} KiB; scaled traffic {fetch_b / 1e9:.1f} GB read + {write_b / 1e9:.1f} GB "
                 f"written = {(fetch_b + write_b) / 1e9:.1f} GB per launch "
                 f"({(fetch_b + write_b) / b['config']['n_atoms']:.0f} B per atom).\n\n")
-        f.write(f"Most of it is the per-pair (m, dm) workspace round trip (2 x {precision * 4} B per active pair "
-                "at k = 32);\n"
-                "the counters see L2-to-fabric requests, which include Infinity Cache hits.\n\n")
+        ws = 2 * 2 * b["config"]["k"] * (precision // 8) * b["config"]["active_pairs_per_atom"]
+        f.write(f"Most of it is the per-pair (m, dm) workspace that pass 1 writes and pass 2 reads back: 2k values per "
+                f"active pair each way, {ws:.0f} B per atom at {b['config']['active_pairs_per_atom']:.2f} active pairs "
+                f"per atom; the per-work-group workspace (about a megabyte per tile) does not stay in the 4 MB L2 of an "
+                f"XCD between the two passes. The rest ({(fetch_b + write_b) / b['config']['n_atoms'] - ws:.0f} B per "
+                f"atom) is neighbour positions, neighbour-list entries, weights missing L2, and outputs. The counters "
+                f"see L2-to-fabric requests, which include Infinity Cache hits.\n\n")
         f.write("traffic_json: " + json.dumps(t) + "\n")
     print(json.dumps(t))
 
@@ -314,7 +318,7 @@ def main() -> int:
     if args.summarize_traffic:
         summarize_traffic(*args.summarize_traffic, copy_bytes=args.calibrate_copy_bytes or 2147483648,
                           command="python3 <repo>/bench.py --steps 1 --warmup 0 --cpu-sample 0 "
-                                  "--calibrate-copy-bytes 2147483648")
+                                  f"--calibrate-copy-bytes 2147483648 --precision {args.precision}")
         return 0
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
