@@ -156,6 +156,51 @@ def test_neighbor_boundary_pairs():
     pot.close()
 
 
+def test_long_rows_small_tiles():
+    """A 12 A cutoff on FCC: about 700 listed neighbours per atom, so tiles of
+    2 centre atoms with about 80 chunks each (weights scaled by 0.3 to keep
+    the descriptor of 620 neighbours at moderate magnitude)."""
+    rng = np.random.default_rng(31)
+    hp = synth.HParams(n_species=3, cutoff=12.0, skin=0.5)
+    pos, box = synth.lattice("fcc", 7, 3.6)
+    pos = pos + rng.normal(0.0, 0.1, pos.shape)
+    types = rng.integers(0, 3, len(pos)).astype(np.int32)
+    g, _ = _compare(hp, synth.random_weights(hp, 4, 0.3), pos, types, box, "long rows")
+    assert g["stats"]["max_row"] > 600 and g["stats"]["tile_atoms"] == 2048 // g["stats"]["max_row"]
+
+
+def test_row_longer_than_cap_is_rejected():
+    """More than 2048 listed neighbours in one row: MLIP_E_NBR_CAP, and the
+    context stays usable for a valid system."""
+    from paper_2608_16329_amd import Potential, MlipError
+    rng = np.random.default_rng(5)
+    box = np.array([20.0, 20.0, 20.0])
+    pos = rng.uniform(0.0, 20.0, (16000, 3))   # about 2300 atoms within 6.5 A of each atom
+    types = np.zeros(len(pos), dtype=np.int32)
+    hp = synth.HParams(n_species=1)
+    log("[nbr] row cap")
+    pot = Potential(hp, synth.random_weights(hp, 0))
+    with pytest.raises(MlipError, match="NBR_CAP"):
+        pot.build_neighbors(to_dev(pos), to_dev(types), box)
+    w = synth.make_workload("fcc-binary-4", seed=2)
+    pot.close()
+    _compare(w.hp, w.weights, w.pos, w.types, w.box, "after cap error")
+
+
+def test_two_atoms_and_pair_at_cutoff():
+    """Degenerate systems: a dimer inside the cutoff, a dimer between r_c and
+    r_c + skin (listed, inactive: zero force)."""
+    hp = synth.HParams(n_species=2)
+    wts = synth.random_weights(hp, 6)
+    box = np.array([16.0, 16.0, 16.0])
+    g, _ = _compare(hp, wts, np.array([[3.0, 3.0, 3.0], [5.5, 4.0, 3.5]]), np.array([0, 1], np.int32), box, "dimer")
+    assert g["stats"]["n_active_pairs"] == 2
+    g, _ = _compare(hp, wts, np.array([[3.0, 3.0, 3.0], [9.2, 3.0, 3.0]]), np.array([1, 1], np.int32), box,
+                    "skin dimer")
+    assert g["stats"]["n_active_pairs"] == 0 and g["stats"]["n_listed_pairs"] == 2
+    assert np.all(g["F"] == 0.0)
+
+
 def test_error_paths():
     from paper_2608_16329_amd import Potential, MlipError
     torch = pytest.importorskip("torch")
