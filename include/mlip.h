@@ -169,6 +169,33 @@ mlip_status mlip_compute(mlip_ctx* ctx, const double* pos_dev, double* energy_de
  */
 mlip_status mlip_get_neighbors(mlip_ctx* ctx, int64_t* offsets_host, int32_t* idx_host);
 
+/*
+ * Fusion configuration of mlip_compute (Section 3.4, Table "Configurable
+ * fusion"); all three give the same results up to rounding.
+ *   MLIP_FUSION_CACHED     one kernel: pass 1 keeps the encoder output and its
+ *                          radial derivative per pair in a fixed-size
+ *                          per-work-group workspace until pass 2 (default)
+ *   MLIP_FUSION_RECOMPUTE  one kernel: pass 2 recomputes the encoder (the
+ *                          paper's mega-fusion); no workspace traffic, twice
+ *                          the encoder work
+ *   MLIP_FUSION_PARTIAL    three kernels (Eqs. 1-5; Eq. 6; Eqs. 7-10, the
+ *                          paper's partial fusion): G_i and then dE/dG_i go
+ *                          through HBM, (l_max+1) k values per atom, which the
+ *                          context allocates at the next mlip_compute
+ */
+typedef enum {
+  MLIP_FUSION_CACHED = 0,
+  MLIP_FUSION_RECOMPUTE = 1,
+  MLIP_FUSION_PARTIAL = 2
+} mlip_fusion;
+
+/*
+ * Select the fusion configuration for later mlip_compute calls.  The
+ * configurations other than MLIP_FUSION_CACHED exist for k = 32.
+ * Errors: MLIP_E_ARG (unknown value, or k != 32 for a non-default one).
+ */
+mlip_status mlip_set_fusion(mlip_ctx* ctx, int32_t fusion);
+
 /* Device memory held by the context, in bytes. */
 mlip_status mlip_memory_bytes(const mlip_ctx* ctx, size_t* bytes);
 

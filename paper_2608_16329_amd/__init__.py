@@ -54,6 +54,10 @@ class Potential:
         return binding.mlip_compute(self.ctx, pos.data_ptr(), energy.data_ptr() if energy is not None else None,
                                     forces.data_ptr(), virial.data_ptr() if virial is not None else None, totals)
 
+    def set_fusion(self, fusion: int) -> None:
+        """binding.MLIP_FUSION_CACHED (default), _RECOMPUTE or _PARTIAL."""
+        binding.mlip_set_fusion(self.ctx, fusion)
+
     def neighbors(self):
         return binding.mlip_get_neighbors(self.ctx)
 

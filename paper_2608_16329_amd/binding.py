@@ -24,7 +24,9 @@ STATUS = {0: "MLIP_OK", -1: "MLIP_E_ARG", -2: "MLIP_E_OOM", -3: "MLIP_E_HIP", -4
 # Every symbol include/mlip.h declares.
 EXPORTED = ["mlip_weight_count", "mlip_create", "mlip_build_neighbors", "mlip_compute", "mlip_get_neighbors",
             "mlip_memory_bytes", "mlip_get_stats", "mlip_last_error", "mlip_destroy", "mlip_md_set_masses",
-            "mlip_md_first_half", "mlip_md_second_half", "mlip_md_kinetic"]
+            "mlip_md_first_half", "mlip_md_second_half", "mlip_md_kinetic", "mlip_set_fusion"]
+
+MLIP_FUSION_CACHED, MLIP_FUSION_RECOMPUTE, MLIP_FUSION_PARTIAL = 0, 1, 2
 
 
 class mlip_hparams(ctypes.Structure):
@@ -73,6 +75,7 @@ def _load() -> ctypes.CDLL:
         "mlip_md_first_half": (st, [vp, vp, vp, vp, ctypes.c_double, vp, dp]),
         "mlip_md_second_half": (st, [vp, vp, vp, ctypes.c_double]),
         "mlip_md_kinetic": (st, [vp, vp, dp]),
+        "mlip_set_fusion": (st, [vp, ctypes.c_int32]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -141,6 +144,10 @@ def mlip_get_neighbors(ctx: int):
     _check(ctx, _lib.mlip_get_neighbors(ctx, off.ctypes.data_as(ctypes.POINTER(ctypes.c_int64)),
                                         idx.ctypes.data_as(ctypes.POINTER(ctypes.c_int32))))
     return off, idx[:n["n_listed_pairs"]]
+
+
+def mlip_set_fusion(ctx: int, fusion: int) -> None:
+    _check(ctx, _lib.mlip_set_fusion(ctx, int(fusion)))
 
 
 def mlip_memory_bytes(ctx: int) -> int:

@@ -409,7 +409,21 @@ mlip_status mlip_compute(mlip_ctx* ctx, const double* pos_dev, double* energy_de
     a.tile_start[sp_i] = t;
     if (sp_i < a.C) t += (ctx->species_start[sp_i + 1] - ctx->species_start[sp_i] + ctx->tile_atoms - 1) / ctx->tile_atoms;
   }
-  if (ctx->n_tiles > 0) MLIP_HIP(ctx, launch_fused(ctx->hp.k, ctx->hp.precision, a, ctx->n_blocks, s));
+  if (ctx->fusion == MLIP_FUSION_PARTIAL) {
+    const size_t need = size_t(n) * size_t((ctx->hp.lmax + 1) * ctx->hp.k) * ctx->elem_bytes;
+    MLIP_TRY(ensure(ctx, &ctx->d_gbuf, &ctx->cap_gbuf, need, "descriptor buffer"));
+    a.gbuf = ctx->d_gbuf;
+  }
+  if (ctx->n_tiles > 0) {
+    const int k = ctx->hp.k, prec = ctx->hp.precision;
+    if (ctx->fusion == MLIP_FUSION_PARTIAL) {
+      MLIP_HIP(ctx, launch_fused(k, prec, 2, a, ctx->n_blocks, s));
+      MLIP_HIP(ctx, launch_fused(k, prec, 3, a, ctx->n_blocks, s));
+      MLIP_HIP(ctx, launch_fused(k, prec, 4, a, ctx->n_blocks, s));
+    } else {
+      MLIP_HIP(ctx, launch_fused(k, prec, ctx->fusion == MLIP_FUSION_RECOMPUTE ? 1 : 0, a, ctx->n_blocks, s));
+    }
+  }
   if (totals_host) {
     MLIP_HIP(ctx, hipMemcpyAsync(totals_host, ctx->d_totals, 10 * sizeof(double), hipMemcpyDeviceToHost, s));
     MLIP_HIP(ctx, hipStreamSynchronize(s));
@@ -438,6 +452,17 @@ mlip_status mlip_get_neighbors(mlip_ctx* ctx, int64_t* offsets_host, int32_t* id
     const int64_t i = perm[size_t(a)];
     std::memcpy(idx_host + offsets_host[i], idx.data() + off[size_t(a)], size_t(len[size_t(i)]) * sizeof(int32_t));
   }
+  return MLIP_OK;
+}
+
+mlip_status mlip_set_fusion(mlip_ctx* ctx, int32_t fusion) {
+  if (!ctx) return MLIP_E_ARG;
+  ctx->err.clear();
+  if (fusion != MLIP_FUSION_CACHED && fusion != MLIP_FUSION_RECOMPUTE && fusion != MLIP_FUSION_PARTIAL)
+    return fail(ctx, MLIP_E_ARG, "unknown fusion configuration");
+  if (fusion != MLIP_FUSION_CACHED && ctx->hp.k != 32)
+    return fail(ctx, MLIP_E_ARG, "the recompute and three-kernel configurations exist for k = 32 only");
+  ctx->fusion = fusion;
   return MLIP_OK;
 }
 
@@ -479,7 +504,7 @@ void mlip_destroy(mlip_ctx* ctx) {
   void* bufs[] = {ctx->d_enc, ctx->d_head, ctx->d_qc, ctx->d_inv_mass, ctx->d_types, ctx->d_perm,
                   ctx->d_key, ctx->d_spos, ctx->d_rowcnt, ctx->d_offsets, ctx->d_idx, ctx->d_cell_count,
                   ctx->d_cell_start, ctx->d_scan_tmp, ctx->d_ws, ctx->d_totals, ctx->d_counters,
-                  ctx->d_flags, ctx->d_reduce};
+                  ctx->d_flags, ctx->d_reduce, ctx->d_gbuf};
   for (void* p : bufs)
     if (p) (void)hipFree(p);
   (void)hipGetLastError();

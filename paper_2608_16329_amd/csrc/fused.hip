@@ -228,76 +228,61 @@ __device__ __forceinline__ PairPos load_pair_pos(const FusedArgs& A, const Smem<
   return p;
 }
 
-// Pass 1 on one chunk: encoder forward + tangent, moment accumulation and
-// the workspace write of (m, dm).
-template <int K, int TM, typename R, int NW>
-__device__ void pass1_chunk(const FusedArgs& A, Smem<K, TM, R, NW>& S, int ch, const PairPos pp, R* __restrict__ wsc) {
-  constexpr int KT = K / 16;
-  const int lane = threadIdx.x & 63, g = lane >> 4, c = lane & 15;
-  const int start = S.ch_start[ch], count = S.ch_count[ch];
-  const int sj = S.ch_s[ch], si = S.tile_species;
-  const int tau = A.enc_cond == 2 ? si * A.C + sj : (A.enc_cond == 1 ? sj : 0);
-  const R* __restrict__ tab = static_cast<const R*>(A.enc) + (long long)tau * A.enc_stride;
-
-  // geometry of the pair in column c (Eq. 1), in float64
-  const bool valid = c < count;
-  double uxd = 1.0, uyd = 0.0, uzd = 0.0, rd = 1.0, fcd = 0.0;
-  int atom = -1;
-  if (valid) {
-    atom = S.pair_a[start + c];
-    const double dx = fold(pp.x - S.tpos[atom][0], A.box[0], A.inv_box[0]);
-    const double dy = fold(pp.y - S.tpos[atom][1], A.box[1], A.inv_box[1]);
-    const double dz = fold(pp.z - S.tpos[atom][2], A.box[2], A.inv_box[2]);
-    rd = sqrt(dx * dx + dy * dy + dz * dz);
-    const double ir = 1.0 / rd;
-    uxd = dx * ir; uyd = dy * ir; uzd = dz * ir;
-    fcd = 0.5 * (1.0 + cos(M_PI * rd / A.rc));
-  }
-  const R r = R(rd), ux = R(uxd), uy = R(uyd), uz = R(uzd), fc = R(fcd);
-
-  // Weight fragments stream from L2 in 16-byte loads (VW fragments of
-  // consecutive output tiles per lane) through register rings, issued
-  // several k-steps ahead of the MFMAs that consume them.
-  constexpr int VW = 16 / int(sizeof(R));   // fragments per load
-  constexpr int NH = 8 / VW;                // loads per hidden-layer k-step
-  constexpr int VO = KT < VW ? KT : VW;     // fragments per output-layer load
-  constexpr int NO = KT / VO;               // loads per output-layer k-step
-  // ring depths: with two wavefronts per SIMD (NW = 8) the other wavefront
-  // covers part of the latency and registers are scarcer
-  constexpr int kRing = (sizeof(R) == 8 || NW == 8) ? 3 : 4;
-  constexpr int kRingOut = (sizeof(R) == 8 || NW == 8) ? 3 : 6;
+// Weight-fragment streaming of the encoder products: fragments of VW
+// consecutive output tiles per 16-byte load, through register rings issued
+// kRing - 1 k-steps ahead of the MFMAs that consume them.
+template <int K, typename R>
+struct Stream {
+  static constexpr int KT = K / 16;
+  static constexpr int VW = 16 / int(sizeof(R));  // fragments per load
+  static constexpr int NH = 8 / VW;               // loads per hidden-layer k-step
+  static constexpr int VO = KT < VW ? KT : VW;    // fragments per output-layer load
+  static constexpr int NO = KT / VO;              // loads per output-layer k-step
+  static constexpr int kRing = 3;
   typedef R vh_t __attribute__((ext_vector_type(VW)));
   typedef R vo_t __attribute__((ext_vector_type(VO)));
-  vh_t wb[kRing][NH];
-  vo_t wo[kRingOut][NO];
-  auto prefetch_hidden = [&](const R* L) {
-    const vh_t* __restrict__ f = reinterpret_cast<const vh_t*>(L) + lane;
-#pragma unroll
-    for (int p = 0; p < kRing - 1; ++p)
-#pragma unroll
-      for (int u = 0; u < NH; ++u) wb[p][u] = f[(p * NH + u) * 64];
-  };
-  auto prefetch_out = [&](const R* L) {
-    const vo_t* __restrict__ f = reinterpret_cast<const vo_t*>(L) + lane;
-#pragma unroll
-    for (int p = 0; p < kRingOut - 1; ++p)
-#pragma unroll
-      for (int u = 0; u < NO; ++u) wo[p][u] = f[(p * NO + u) * 64];
-  };
-  // float32 with one wavefront per SIMD issues each product's first
-  // fragments before the activation work in front of it; the other
-  // configurations have no registers to spare for that
-  constexpr bool kEarly = sizeof(R) == 4 && NW == 4;
-  const R* __restrict__ layer = tab + 2 * kEncWidth;
-  if (kEarly) {
-    if (A.enc_hidden > 1)
-      prefetch_hidden(layer);
-    else
-      prefetch_out(layer);
-  }
+};
 
-  // first layer (scalar input), rows in = 16T + drow(i, g) of column c
-  R h[8][4], dh[8][4];
+// Distance of the pair in column c of chunk ch (Eq. 1), in float64; 1 for
+// the padding columns of a partial chunk.
+template <int K, int TM, typename R, int NW>
+__device__ __forceinline__ double pair_distance(const FusedArgs& A, const Smem<K, TM, R, NW>& S, int ch,
+                                                const PairPos& pp, double* ux, double* uy, double* uz, int* atom) {
+  const int c = threadIdx.x & 15;
+  *ux = 1.0; *uy = 0.0; *uz = 0.0; *atom = -1;
+  if (c >= S.ch_count[ch]) return 1.0;
+  const int a = S.pair_a[S.ch_start[ch] + c];
+  const double dx = fold(pp.x - S.tpos[a][0], A.box[0], A.inv_box[0]);
+  const double dy = fold(pp.y - S.tpos[a][1], A.box[1], A.inv_box[1]);
+  const double dz = fold(pp.z - S.tpos[a][2], A.box[2], A.inv_box[2]);
+  const double r = sqrt(dx * dx + dy * dy + dz * dz);
+  const double ir = 1.0 / r;
+  *ux = dx * ir; *uy = dy * ir; *uz = dz * ir;
+  *atom = a;
+  return r;
+}
+
+// Encoder table of chunk ch (pair conditioning, Section 3.2).
+template <int K, int TM, typename R, int NW>
+__device__ __forceinline__ const R* chunk_table(const FusedArgs& A, const Smem<K, TM, R, NW>& S, int ch) {
+  const int sj = S.ch_s[ch], si = S.tile_species;
+  const int tau = A.enc_cond == 2 ? si * A.C + sj : (A.enc_cond == 1 ? sj : 0);
+  return static_cast<const R*>(A.enc) + (long long)tau * A.enc_stride;
+}
+
+// Encoder forward and tangent (Eq. 2 and its derivative in r) up to the last
+// hidden layer for the 16 pairs of a chunk: the first layer (scalar input)
+// from the LDS copy of (w0, b0), then the residual hidden layers Z = W H as
+// 8 x 32 MFMA steps whose forward and tangent columns share each weight
+// fragment.  On return h[T][i], dh[T][i] hold rows 16T + drow(i, g) of
+// column c; the result is the output-layer section of the table.
+template <int K, int TM, typename R, int NW>
+__device__ __forceinline__ const R* encoder_hidden(const FusedArgs& A, const Smem<K, TM, R, NW>& S, int sj, R r,
+                                                   const R* __restrict__ tab, R (&h)[8][4], R (&dh)[8][4]) {
+  typedef Stream<K, R> St;
+  typedef typename St::vh_t vh_t;
+  constexpr int NH = St::NH, VW = St::VW, kRing = St::kRing;
+  const int lane = threadIdx.x & 63, g = lane >> 4;
 #pragma unroll
   for (int T = 0; T < 8; ++T)
 #pragma unroll
@@ -308,13 +293,15 @@ __device__ void pass1_chunk(const FusedArgs& A, Smem<K, TM, R, NW>& S, int ch, c
       h[T][i] = z * s;
       dh[T][i] = s * (R(1) + z * (R(1) - s)) * w0;
     }
-
-  // residual hidden layers: Z = W H as 8 x 32 MFMA steps, forward and
-  // tangent columns share each weight fragment
+  const R* __restrict__ layer = tab + 2 * kEncWidth;
   for (int t = 1; t < A.enc_hidden; ++t) {
     const vh_t* __restrict__ frag = reinterpret_cast<const vh_t*>(layer) + lane;
     const R* __restrict__ bias = layer + kEncWidth * kEncWidth;
-    if (!kEarly) prefetch_hidden(layer);
+    vh_t wb[kRing][NH];
+#pragma unroll
+    for (int p = 0; p < kRing - 1; ++p)
+#pragma unroll
+      for (int u = 0; u < NH; ++u) wb[p][u] = frag[(p * NH + u) * 64];
     // the forward accumulators start from the bias; the tangent has none
     v4<R> acc[8], dacc[8];
 #pragma unroll
@@ -340,12 +327,6 @@ __device__ void pass1_chunk(const FusedArgs& A, Smem<K, TM, R, NW>& S, int ch, c
       __builtin_amdgcn_sched_barrier(0);
     }
     layer += kEncWidth * kEncWidth + kEncWidth;
-    if (kEarly) {
-      if (t + 1 < A.enc_hidden)
-        prefetch_hidden(layer);
-      else
-        prefetch_out(layer);
-    }
 #pragma unroll
     for (int To = 0; To < 8; ++To)
 #pragma unroll
@@ -356,46 +337,127 @@ __device__ void pass1_chunk(const FusedArgs& A, Smem<K, TM, R, NW>& S, int ch, c
         dh[To][q] += s * (R(1) + z * (R(1) - s)) * dacc[To][q];
       }
   }
+  return layer;
+}
 
-  // output layer with pairs as rows: m[pair drow(q, g)][16Tc + c]; even and
-  // odd k-steps accumulate separately so 4 KT independent MFMA chains are in
-  // flight
-  v4<R> mo[KT], dmo[KT];
-  {
-    const R* __restrict__ bout = layer + K * kEncWidth;
-    v4<R> mo2[2][KT], dmo2[2][KT];
+// Encoder output layer with pairs as rows: mo[Tc] register q holds
+// m[pair drow(q, g)][16Tc + c] (dmo the same for the tangent).  Even and odd
+// k-steps accumulate separately so 4 KT independent MFMA chains are in
+// flight.
+template <int K, typename R>
+__device__ __forceinline__ void encoder_out_rows(const R* __restrict__ layer, const R (&h)[8][4], const R (&dh)[8][4],
+                                                 v4<R> (&mo)[K / 16], v4<R> (&dmo)[K / 16]) {
+  typedef Stream<K, R> St;
+  typedef typename St::vo_t vo_t;
+  constexpr int KT = St::KT, NO = St::NO, VO = St::VO, kRing = St::kRing;
+  const int lane = threadIdx.x & 63, c = lane & 15;
+  const R* __restrict__ bout = layer + K * kEncWidth;
+  v4<R> mo2[2][KT], dmo2[2][KT];
 #pragma unroll
-    for (int Tc = 0; Tc < KT; ++Tc) {
-      const R b = bout[16 * Tc + c];
-      mo2[0][Tc] = v4<R>{b, b, b, b};
-      mo2[1][Tc] = v4<R>{0, 0, 0, 0};
-      dmo2[0][Tc] = v4<R>{0, 0, 0, 0};
-      dmo2[1][Tc] = v4<R>{0, 0, 0, 0};
-    }
-    if (!kEarly) prefetch_out(layer);
-    const vo_t* __restrict__ frag = reinterpret_cast<const vo_t*>(layer) + lane;
-#pragma unroll
-    for (int ks = 0; ks < 32; ++ks) {
-      if (ks + kRingOut - 1 < 32) {
-#pragma unroll
-        for (int u = 0; u < NO; ++u) wo[(ks + kRingOut - 1) % kRingOut][u] = frag[((ks + kRingOut - 1) * NO + u) * 64];
-      }
-      __builtin_amdgcn_sched_barrier(0);
-      const int T = ks >> 2, i = ks & 3;
-#pragma unroll
-      for (int Tc = 0; Tc < KT; ++Tc) {
-        const R wv = wo[ks % kRingOut][Tc / VO][Tc % VO];
-        mo2[ks & 1][Tc] = mfma(h[T][i], wv, mo2[ks & 1][Tc]);
-        dmo2[ks & 1][Tc] = mfma(dh[T][i], wv, dmo2[ks & 1][Tc]);
-      }
-      __builtin_amdgcn_sched_barrier(0);
-    }
-#pragma unroll
-    for (int Tc = 0; Tc < KT; ++Tc) {
-      mo[Tc] = mo2[0][Tc] + mo2[1][Tc];
-      dmo[Tc] = dmo2[0][Tc] + dmo2[1][Tc];
-    }
+  for (int Tc = 0; Tc < KT; ++Tc) {
+    const R b = bout[16 * Tc + c];
+    mo2[0][Tc] = v4<R>{b, b, b, b};
+    mo2[1][Tc] = v4<R>{0, 0, 0, 0};
+    dmo2[0][Tc] = v4<R>{0, 0, 0, 0};
+    dmo2[1][Tc] = v4<R>{0, 0, 0, 0};
   }
+  const vo_t* __restrict__ frag = reinterpret_cast<const vo_t*>(layer) + lane;
+  vo_t wo[kRing][NO];
+#pragma unroll
+  for (int p = 0; p < kRing - 1; ++p)
+#pragma unroll
+    for (int u = 0; u < NO; ++u) wo[p][u] = frag[(p * NO + u) * 64];
+#pragma unroll
+  for (int ks = 0; ks < 32; ++ks) {
+    if (ks + kRing - 1 < 32) {
+#pragma unroll
+      for (int u = 0; u < NO; ++u) wo[(ks + kRing - 1) % kRing][u] = frag[((ks + kRing - 1) * NO + u) * 64];
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    const int T = ks >> 2, i = ks & 3;
+#pragma unroll
+    for (int Tc = 0; Tc < KT; ++Tc) {
+      const R wv = wo[ks % kRing][Tc / VO][Tc % VO];
+      mo2[ks & 1][Tc] = mfma(h[T][i], wv, mo2[ks & 1][Tc]);
+      dmo2[ks & 1][Tc] = mfma(dh[T][i], wv, dmo2[ks & 1][Tc]);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+  }
+#pragma unroll
+  for (int Tc = 0; Tc < KT; ++Tc) {
+    mo[Tc] = mo2[0][Tc] + mo2[1][Tc];
+    dmo[Tc] = dmo2[0][Tc] + dmo2[1][Tc];
+  }
+}
+
+// Encoder output layer with pairs as columns (the same fragments serve as
+// the A operand): register q of lane (g, c) for output tile Tc holds
+// m[pair c][16Tc + drow(q, g)], which is exactly the B operand of pass 2's
+// W m product.
+template <int K, typename R>
+__device__ __forceinline__ void encoder_out_cols(const R* __restrict__ layer, const R (&h)[8][4], const R (&dh)[8][4],
+                                                 R (&mB)[K / 16][4], R (&dmB)[K / 16][4]) {
+  typedef Stream<K, R> St;
+  typedef typename St::vo_t vo_t;
+  constexpr int KT = St::KT, NO = St::NO, VO = St::VO, kRing = St::kRing;
+  const int lane = threadIdx.x & 63, g = lane >> 4;
+  const R* __restrict__ bout = layer + K * kEncWidth;
+  v4<R> acc[KT], dacc[KT];
+#pragma unroll
+  for (int Tc = 0; Tc < KT; ++Tc) {
+    acc[Tc] = v4<R>{bout[16 * Tc + drow<R>(0, g)], bout[16 * Tc + drow<R>(1, g)], bout[16 * Tc + drow<R>(2, g)],
+                    bout[16 * Tc + drow<R>(3, g)]};
+    dacc[Tc] = v4<R>{0, 0, 0, 0};
+  }
+  const vo_t* __restrict__ frag = reinterpret_cast<const vo_t*>(layer) + lane;
+  vo_t wo[kRing][NO];
+#pragma unroll
+  for (int p = 0; p < kRing - 1; ++p)
+#pragma unroll
+    for (int u = 0; u < NO; ++u) wo[p][u] = frag[(p * NO + u) * 64];
+#pragma unroll
+  for (int ks = 0; ks < 32; ++ks) {
+    if (ks + kRing - 1 < 32) {
+#pragma unroll
+      for (int u = 0; u < NO; ++u) wo[(ks + kRing - 1) % kRing][u] = frag[((ks + kRing - 1) * NO + u) * 64];
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    const int T = ks >> 2, i = ks & 3;
+#pragma unroll
+    for (int Tc = 0; Tc < KT; ++Tc) {
+      const R wv = wo[ks % kRing][Tc / VO][Tc % VO];
+      acc[Tc] = mfma(wv, h[T][i], acc[Tc]);
+      dacc[Tc] = mfma(wv, dh[T][i], dacc[Tc]);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+  }
+#pragma unroll
+  for (int Tc = 0; Tc < KT; ++Tc)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      mB[Tc][q] = acc[Tc][q];
+      dmB[Tc][q] = dacc[Tc][q];
+    }
+}
+
+// Pass 1 on one chunk: encoder forward + tangent, moment accumulation and,
+// when kWs, the workspace write of (m, dm).
+template <int K, int TM, typename R, int NW, bool kWs>
+__device__ void pass1_chunk(const FusedArgs& A, Smem<K, TM, R, NW>& S, int ch, const PairPos pp, R* __restrict__ wsc) {
+  constexpr int KT = K / 16;
+  const int lane = threadIdx.x & 63, g = lane >> 4, c = lane & 15;
+  const int start = S.ch_start[ch], count = S.ch_count[ch];
+
+  double uxd, uyd, uzd;
+  int atom;
+  const double rd = pair_distance(A, S, ch, pp, &uxd, &uyd, &uzd, &atom);
+  const double fcd = atom >= 0 ? 0.5 * (1.0 + cos(M_PI * rd / A.rc)) : 0.0;
+  const R r = R(rd), ux = R(uxd), uy = R(uyd), uz = R(uzd), fc = R(fcd);
+
+  R h[8][4], dh[8][4];
+  const R* __restrict__ layer = encoder_hidden(A, S, S.ch_s[ch], r, chunk_table(A, S, ch), h, dh);
+  v4<R> mo[KT], dmo[KT];
+  encoder_out_rows<K, R>(layer, h, dh, mo, dmo);
 
   // moment: P[mm][col] += sum_pairs fc * a_mm(u) * m[pair][col], one MFMA
   // product per centre atom present in the chunk (pairs of other atoms are
@@ -432,17 +494,19 @@ __device__ void pass1_chunk(const FusedArgs& A, Smem<K, TM, R, NW>& S, int ch, c
       for (int q = 0; q < 4; ++q) atomicAdd(&S.P[a][drow<R>(q, g)][16 * Tc + c], pacc[Tc][q]);
   }
 
-  // workspace in the B-operand order pass 2 loads, contiguous per lane:
-  // lane 16 g' + c' holds m[pair c'][16Tc + drow(i, g')] at 4 KT lane' +
-  // 4 Tc + i (then the same for dm)
+  if (kWs) {
+    // workspace in the B-operand order pass 2 loads, contiguous per lane:
+    // lane 16 g' + c' holds m[pair c'][16Tc + drow(i, g')] at 4 KT lane' +
+    // 4 Tc + i (then the same for dm)
 #pragma unroll
-  for (int Tc = 0; Tc < KT; ++Tc)
+    for (int Tc = 0; Tc < KT; ++Tc)
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const int off = (16 * gof<R>(c) + drow<R>(q, g)) * (4 * KT) + Tc * 4 + qof<R>(c);
-      wsc[off] = mo[Tc][q];
-      wsc[K * 16 + off] = dmo[Tc][q];
-    }
+      for (int q = 0; q < 4; ++q) {
+        const int off = (16 * gof<R>(c) + drow<R>(q, g)) * (4 * KT) + Tc * 4 + qof<R>(c);
+        wsc[off] = mo[Tc][q];
+        wsc[K * 16 + off] = dmo[Tc][q];
+      }
+  }
 }
 
 // Inputs of pass 2 for one chunk: the workspace tiles (m, dm) in B-operand
@@ -476,6 +540,20 @@ __device__ __forceinline__ void pass2_load(const FusedArgs& A, const Smem<K, TM,
       in.dmB[Tc][i] = vd[(Tc * 4 + i) / VW][(Tc * 4 + i) % VW];
     }
   in.pp = load_pair_pos(A, S, ch);
+}
+
+// Inputs of pass 2 for one chunk by recomputing the encoder instead of
+// reading the workspace (the paper's mega-fusion, Section 3.4).
+template <int K, int TM, typename R, int NW>
+__device__ __forceinline__ void pass2_recompute(const FusedArgs& A, const Smem<K, TM, R, NW>& S, int ch,
+                                                const PairPos& pp, Pass2In<K, R>& in) {
+  double ux, uy, uz;
+  int atom;
+  const R r = R(pair_distance(A, S, ch, pp, &ux, &uy, &uz, &atom));
+  R h[8][4], dh[8][4];
+  const R* __restrict__ layer = encoder_hidden(A, S, S.ch_s[ch], r, chunk_table(A, S, ch), h, dh);
+  encoder_out_cols<K, R>(layer, h, dh, in.mB, in.dmB);
+  in.pp = pp;
 }
 
 // Pass 2 on one chunk: W contractions, partial forces and scatter.
@@ -583,13 +661,38 @@ __device__ void pass2_chunk(const FusedArgs& A, Smem<K, TM, R, NW>& S, int ch, c
   }
 }
 
+// Descriptor value x[in] = vec(G)[in] of tile atom a (Eq. 5): the l = 0
+// block is linear, blocks l >= 1 are squared norms over their 2l + 1 rows.
+template <int K, int TM, typename R, int NW>
+__device__ __forceinline__ R descriptor_value(const Smem<K, TM, R, NW>& S, int a, int in) {
+  const int l = in / K, col = in % K;
+  if (l == 0) return S.P[a][0][col];
+  R v = 0;
+  for (int mm = l * l; mm < (l + 1) * (l + 1); ++mm) v += S.P[a][mm][col] * S.P[a][mm][col];
+  return v;
+}
+
+// W = dE/dP (Eq. 7) for tile atom a from dE/dx[in]: W[0][col] = dE/dG[0][col],
+// W[m][col] = 2 dE/dG[l][col] P[m][col]; overwrites P.
+template <int K, int TM, typename R, int NW>
+__device__ __forceinline__ void adjoint_from_grad(Smem<K, TM, R, NW>& S, int a, int in, R d) {
+  const int l = in / K, col = in % K;
+  if (l == 0) {
+    S.P[a][0][col] = d;
+  } else {
+    for (int mm = l * l; mm < (l + 1) * (l + 1); ++mm) S.P[a][mm][col] *= R(2) * d;
+  }
+}
+
 // Descriptor (Eq. 5), head forward and backward (Eq. 6) and W = dE/dP
 // (Eq. 7) for the tile on MFMA: the tile's atoms are the 16 columns of every
 // product and wavefront w < 4 owns rows 16w..16w+15 of each 64-wide layer.
 // Activations live in LDS feature-major ([feature][atom]) so that B-operand
 // reads are contiguous; pre-activations stay in registers for the backward
-// pass.
-template <int K, int TM, typename R, int NW>
+// pass.  With kRegress (the regression kernel of the three-kernel
+// configuration) the descriptor comes from HBM and dE/dx goes back to HBM in
+// its place instead of forming W.
+template <int K, int TM, typename R, int NW, bool kRegress>
 __device__ void head_stage(const FusedArgs& A, Smem<K, TM, R, NW>& S) {
   constexpr int RW = kHeadWidth;
   constexpr int HS = 2 * RW * RW + RW;  // one hidden layer: A_t and A_t^T fragments, c_t
@@ -597,17 +700,11 @@ __device__ void head_stage(const FusedArgs& A, Smem<K, TM, R, NW>& S) {
   const int na = S.na;
   const int nin = (A.lmax + 1) * K;
   const int tin = nin / 16;
+  R* __restrict__ gbuf = kRegress ? static_cast<R*>(A.gbuf) + (long long)S.a0 * nin : nullptr;
   for (int u = tid; u < 16 * nin; u += (64 * NW)) {
     const int a = u & 15, in = u >> 4;
     R v = 0;
-    if (a < na) {
-      const int l = in / K, col = in % K;
-      if (l == 0) {
-        v = S.P[a][0][col];
-      } else {
-        for (int mm = l * l; mm < (l + 1) * (l + 1); ++mm) v += S.P[a][mm][col] * S.P[a][mm][col];
-      }
-    }
+    if (a < na) v = kRegress ? gbuf[(long long)a * nin + in] : descriptor_value(S, a, in);
     S.u.hd.xT[in][a] = v;
   }
   __syncthreads();
@@ -703,12 +800,10 @@ __device__ void head_stage(const FusedArgs& A, Smem<K, TM, R, NW>& S) {
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
         const int in = 16 * tt + drow<R>(q, g);
-        const int l = in / K, col = in % K;
-        if (l == 0) {
-          S.P[c][0][col] = acc[q];
-        } else {
-          for (int mm = l * l; mm < (l + 1) * (l + 1); ++mm) S.P[c][mm][col] *= R(2) * acc[q];
-        }
+        if (kRegress)
+          gbuf[(long long)c * nin + in] = acc[q];
+        else
+          adjoint_from_grad(S, c, in, acc[q]);
       }
     }
   }
@@ -716,7 +811,27 @@ __device__ void head_stage(const FusedArgs& A, Smem<K, TM, R, NW>& S) {
 #undef ROW
 }
 
+// First-layer weights (w0, b0) of the tile's encoder tables, one per
+// neighbour species, into LDS.
 template <int K, int TM, typename R, int NW>
+__device__ __forceinline__ void stage_first_layer(const FusedArgs& A, Smem<K, TM, R, NW>& S,
+                                                  const R* __restrict__ enc) {
+  for (int u = threadIdx.x; u < A.C * 2 * kEncWidth; u += 64 * NW) {
+    const int sj = u / (2 * kEncWidth), rem = u % (2 * kEncWidth);
+    const int si = S.tile_species;
+    const int tau = A.enc_cond == 2 ? si * A.C + sj : (A.enc_cond == 1 ? sj : 0);
+    S.u.l0[sj][rem / kEncWidth][rem % kEncWidth] = enc[(long long)tau * A.enc_stride + rem];
+  }
+}
+
+// What one launch does (Section 3.4 fusion configurations, numbered as in
+// mlip_fusion): the single kernel that caches (m, dm) between its two
+// passes or recomputes them in pass 2, or one of the three kernels of the
+// partial configuration: encoding (Eqs. 1-5, G to HBM), regression (Eq. 6,
+// E and dE/dG to HBM) and derivation (Eqs. 7-10, recomputing P).
+enum Mode { kCached = 0, kRecompute = 1, kEncode = 2, kRegress = 3, kDerive = 4 };
+
+template <int K, int TM, typename R, int NW, int MODE>
 __global__ __launch_bounds__(64 * NW, 1) void k_fused(FusedArgs A) {
   extern __shared__ __align__(16) unsigned char smem_raw[];
   Smem<K, TM, R, NW>& S = *reinterpret_cast<Smem<K, TM, R, NW>*>(smem_raw);
@@ -754,17 +869,6 @@ __global__ __launch_bounds__(64 * NW, 1) void k_fused(FusedArgs A) {
     __syncthreads();
     const int na = S.na;
     const int a0 = S.a0;
-    for (int u = tid; u < A.C * 2 * kEncWidth; u += (64 * NW)) {
-      const int sj = u / (2 * kEncWidth), rem = u % (2 * kEncWidth);
-      const int si = S.tile_species;
-      const int tau = A.enc_cond == 2 ? si * A.C + sj : (A.enc_cond == 1 ? sj : 0);
-      S.u.l0[sj][rem / kEncWidth][rem % kEncWidth] = enc[(long long)tau * A.enc_stride + rem];
-    }
-    if (tid <= TM) {
-      const int k = tid < na ? tid : na;
-      S.ent_base[tid] = int(A.offsets[a0 + k] - A.offsets[a0]);
-      if (tid == 0) S.row_beg[0] = A.offsets[a0];
-    }
     if (tid < TM) {
       if (tid < na) {
         const int o = A.perm[a0 + tid];
@@ -778,6 +882,14 @@ __global__ __launch_bounds__(64 * NW, 1) void k_fused(FusedArgs A) {
 #pragma unroll
       for (int k = 0; k < 9; ++k) S.Wi[tid][k] = 0.0;
       S.Ei[tid] = 0.0;
+    }
+    int nch = 0;
+    if constexpr (MODE != kRegress) {
+    stage_first_layer(A, S, enc);
+    if (tid <= TM) {
+      const int k = tid < na ? tid : na;
+      S.ent_base[tid] = int(A.offsets[a0 + k] - A.offsets[a0]);
+      if (tid == 0) S.row_beg[0] = A.offsets[a0];
     }
     for (int u = tid; u < kMaxSpecies * TM; u += (64 * NW)) S.cnt[u / TM][u % TM] = 0;
     for (int u = tid; u < TM * kAngRows * (K + 1); u += (64 * NW)) (&S.P[0][0][0])[u] = R(0);
@@ -874,22 +986,40 @@ __global__ __launch_bounds__(64 * NW, 1) void k_fused(FusedArgs A) {
     __syncthreads();
 
     // ---- B: pass 1 ---------------------------------------------------------
-    const int nch = S.n_chunks;
+    nch = S.n_chunks;
     {
+      constexpr bool kWs = MODE == kCached || MODE == kDerive;
       PairPos next = wave < nch ? load_pair_pos(A, S, wave) : PairPos{0.0, 0.0, 0.0};
       for (int ch = wave; ch < nch; ch += NW) {
         const PairPos cur = next;
         if (ch + NW < nch) next = load_pair_pos(A, S, ch + NW);
-        pass1_chunk<K, TM, R, NW>(A, S, ch, cur, ws_slot + ch * chunk_elems);
+        pass1_chunk<K, TM, R, NW, kWs>(A, S, ch, cur, ws_slot + ch * chunk_elems);
       }
     }
     __syncthreads();
+    }  // MODE != kRegress
 
     // ---- C: descriptor, head, W ------------------------------------------
-    head_stage<K, TM, R, NW>(A, S);
+    if constexpr (MODE == kCached || MODE == kRecompute) {
+      head_stage<K, TM, R, NW, false>(A, S);
+    } else if constexpr (MODE == kRegress) {
+      head_stage<K, TM, R, NW, true>(A, S);
+    } else {
+      // encoding kernel: G to HBM; derivation kernel: W from dE/dG in HBM
+      const int nin = (A.lmax + 1) * K;
+      R* __restrict__ gbuf = static_cast<R*>(A.gbuf) + (long long)a0 * nin;
+      for (int u = tid; u < na * nin; u += 64 * NW) {
+        const int a = u / nin, in = u % nin;
+        if constexpr (MODE == kEncode)
+          gbuf[u] = descriptor_value(S, a, in);
+        else
+          adjoint_from_grad(S, a, in, gbuf[u]);
+      }
+      __syncthreads();
+    }
 
     // ---- D: pass 2 ---------------------------------------------------------
-    {
+    if constexpr (MODE == kCached || MODE == kDerive) {
       Pass2In<K, R> next;
       if (wave < nch) pass2_load(A, S, wave, ws_slot + wave * chunk_elems, next);
       for (int ch = wave; ch < nch; ch += NW) {
@@ -897,27 +1027,43 @@ __global__ __launch_bounds__(64 * NW, 1) void k_fused(FusedArgs A) {
         if (ch + NW < nch) pass2_load(A, S, ch + NW, ws_slot + (ch + NW) * chunk_elems, next);
         pass2_chunk<K, TM, R, NW>(A, S, ch, cur);
       }
+    } else if constexpr (MODE == kRecompute) {
+      // the head's activations overwrote the first-layer weights in LDS
+      stage_first_layer(A, S, enc);
+      __syncthreads();
+      PairPos next = wave < nch ? load_pair_pos(A, S, wave) : PairPos{0.0, 0.0, 0.0};
+      for (int ch = wave; ch < nch; ch += NW) {
+        const PairPos cur = next;
+        if (ch + NW < nch) next = load_pair_pos(A, S, ch + NW);
+        Pass2In<K, R> in;
+        pass2_recompute(A, S, ch, cur, in);
+        pass2_chunk<K, TM, R, NW>(A, S, ch, in);
+      }
     }
     __syncthreads();
 
     // ---- E: outputs --------------------------------------------------------
+    constexpr bool kEnergy = MODE == kCached || MODE == kRecompute || MODE == kRegress;
+    constexpr bool kForces = MODE == kCached || MODE == kRecompute || MODE == kDerive;
     if (tid < na) {
       const long long o = S.orig[tid];
-      if (A.energy) A.energy[o] = S.Ei[tid];
-      if (A.virial) {
+      if (kEnergy && A.energy) A.energy[o] = S.Ei[tid];
+      if (kForces) {
+        if (A.virial) {
 #pragma unroll
-        for (int k = 0; k < 9; ++k) A.virial[9 * o + k] = S.Wi[tid][k];
+          for (int k = 0; k < 9; ++k) A.virial[9 * o + k] = S.Wi[tid][k];
+        }
+        atomicAdd(&A.forces[3 * o], S.Fi[tid][0]);
+        atomicAdd(&A.forces[3 * o + 1], S.Fi[tid][1]);
+        atomicAdd(&A.forces[3 * o + 2], S.Fi[tid][2]);
       }
-      atomicAdd(&A.forces[3 * o], S.Fi[tid][0]);
-      atomicAdd(&A.forces[3 * o + 1], S.Fi[tid][1]);
-      atomicAdd(&A.forces[3 * o + 2], S.Fi[tid][2]);
     }
-    if (wave == 0) {
+    if (wave == 0 && MODE != kEncode) {
       double v[10];
       const bool own = tid < na;
-      v[0] = own ? S.Ei[tid] : 0.0;
+      v[0] = kEnergy && own ? S.Ei[tid] : 0.0;
 #pragma unroll
-      for (int k = 0; k < 9; ++k) v[1 + k] = own ? S.Wi[tid][k] : 0.0;
+      for (int k = 0; k < 9; ++k) v[1 + k] = kForces && own ? S.Wi[tid][k] : 0.0;
 #pragma unroll
       for (int k = 0; k < 10; ++k)
 #pragma unroll
@@ -929,47 +1075,61 @@ __global__ __launch_bounds__(64 * NW, 1) void k_fused(FusedArgs A) {
           if (tid == k) mine = v[k];
         atomicAdd(&A.totals[tid], mine);
       }
-      if (tid == 0) atomicAdd(&A.counters[0], (unsigned long long)S.n_active);
+      if (tid == 0 && kForces) atomicAdd(&A.counters[0], (unsigned long long)S.n_active);
     }
     __syncthreads();
   }
 }
 
-template <int K, int TM, typename R, int NW>
+template <int K, int TM, typename R, int NW, int MODE>
 hipError_t launch_k(const FusedArgs& a, int n_blocks, hipStream_t s) {
   static_assert(sizeof(Smem<K, TM, R, NW>) <= 160 * 1024, "tile state exceeds the 160 KB LDS of a CU");
   const size_t smem = sizeof(Smem<K, TM, R, NW>);
   static bool attr_set = false;
   if (!attr_set) {
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_fused<K, TM, R, NW>),
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_fused<K, TM, R, NW, MODE>),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, int(smem));
     if (e != hipSuccess) return e;
     attr_set = true;
   }
-  k_fused<K, TM, R, NW><<<dim3(unsigned(n_blocks)), dim3(64 * NW), smem, s>>>(a);
+  k_fused<K, TM, R, NW, MODE><<<dim3(unsigned(n_blocks)), dim3(64 * NW), smem, s>>>(a);
   return hipGetLastError();
+}
+
+template <int K, int TM, typename R, int NW>
+hipError_t launch_mode(int mode, const FusedArgs& a, int n_blocks, hipStream_t s) {
+  switch (mode) {
+    case kCached: return launch_k<K, TM, R, NW, kCached>(a, n_blocks, s);
+    case kRecompute: return launch_k<K, TM, R, NW, kRecompute>(a, n_blocks, s);
+    case kEncode: return launch_k<K, TM, R, NW, kEncode>(a, n_blocks, s);
+    case kRegress: return launch_k<K, TM, R, NW, kRegress>(a, n_blocks, s);
+    case kDerive: return launch_k<K, TM, R, NW, kDerive>(a, n_blocks, s);
+    default: return hipErrorInvalidValue;
+  }
 }
 
 }  // namespace
 
 // Instantiations: k in {16, 32, 64}; float64 with one wavefront per SIMD,
 // float32 with two; 16 atoms per tile except float64 at k = 64, whose moment
-// tiles need 8 to fit in LDS.
+// tiles need 8 to fit in LDS.  The other fusion configurations are built for
+// k = 32 only.
 int fused_tile_max(int k, int precision) { return (k == 64 && precision == 64) ? 8 : 16; }
 
-hipError_t launch_fused(int k, int precision, const FusedArgs& a, int n_blocks, hipStream_t s) {
+hipError_t launch_fused(int k, int precision, int mode, const FusedArgs& a, int n_blocks, hipStream_t s) {
+  if (mode != kCached && k != 32) return hipErrorInvalidValue;
   if (precision == 64) {
     switch (k) {
-      case 16: return launch_k<16, 16, double, 4>(a, n_blocks, s);
-      case 32: return launch_k<32, 16, double, 4>(a, n_blocks, s);
-      case 64: return launch_k<64, 8, double, 4>(a, n_blocks, s);
+      case 16: return launch_k<16, 16, double, 4, kCached>(a, n_blocks, s);
+      case 32: return launch_mode<32, 16, double, 4>(mode, a, n_blocks, s);
+      case 64: return launch_k<64, 8, double, 4, kCached>(a, n_blocks, s);
       default: break;
     }
   } else if (precision == 32) {
     switch (k) {
-      case 16: return launch_k<16, 16, float, 8>(a, n_blocks, s);
-      case 32: return launch_k<32, 16, float, 8>(a, n_blocks, s);
-      case 64: return launch_k<64, 16, float, 8>(a, n_blocks, s);
+      case 16: return launch_k<16, 16, float, 8, kCached>(a, n_blocks, s);
+      case 32: return launch_mode<32, 16, float, 8>(mode, a, n_blocks, s);
+      case 64: return launch_k<64, 16, float, 8, kCached>(a, n_blocks, s);
       default: break;
     }
   }

@@ -54,6 +54,7 @@ struct FusedArgs {
   unsigned long long* counters;  // [0] active pairs (zeroed before launch)
   void* ws;                   // per-block workspace
   long long ws_slot;          // values per block slot
+  void* gbuf;                 // [n][(lmax+1) k] by sorted slot: G, then dE/dG (three-kernel configuration)
   double box[3];
   double inv_box[3];
   double rc, rc2;
@@ -133,6 +134,9 @@ struct mlip_ctx {
   int tile_atoms = 0;
   int64_t n_tiles = 0;
   int n_blocks = 0;
+  int fusion = 0;                   // mlip_fusion
+  unsigned char* d_gbuf = nullptr;  // G / dE/dG per atom (three-kernel configuration), cap_gbuf bytes
+  size_t cap_gbuf = 0;
 };
 
 namespace mlip {
@@ -161,8 +165,10 @@ hipError_t launch_fill_i32(int32_t* p, int64_t n, int32_t v, hipStream_t s);
 hipError_t launch_fill_f64(double* p, int64_t n, double v, hipStream_t s);
 hipError_t launch_fill_u64(unsigned long long* p, int64_t n, hipStream_t s);
 
-// fused.hip (k 16, 32 or 64; precision 64 or 32)
-hipError_t launch_fused(int k, int precision, const FusedArgs& a, int n_blocks, hipStream_t s);
+// fused.hip (k 16, 32 or 64; precision 64 or 32; mode: 0 cached, 1 recompute,
+// 2 encoding, 3 regression, 4 derivation kernel of the three-kernel split;
+// modes other than 0 for k = 32 only)
+hipError_t launch_fused(int k, int precision, int mode, const FusedArgs& a, int n_blocks, hipStream_t s);
 int fused_tile_max(int k, int precision);  // centre atoms per tile of that instantiation
 
 // md.hip

@@ -25,11 +25,14 @@ def to_dev(a, dtype=None):
     return t.to("cuda:0").contiguous()
 
 
-def gpu_eval(hp, weights, pos, types, box, want_energy=True, want_virial=True):
-    """Build neighbours and evaluate once on the GPU; returns host arrays."""
+def gpu_eval(hp, weights, pos, types, box, want_energy=True, want_virial=True, fusion=0):
+    """Build neighbours and evaluate once on the GPU (in the given fusion
+    configuration); returns host arrays."""
     torch = torch_mod()
     from paper_2608_16329_amd import Potential
     pot = Potential(hp, weights)
+    if fusion:
+        pot.set_fusion(fusion)
     p = to_dev(pos, torch.float64)
     t = to_dev(types.astype(np.int32))
     pot.build_neighbors(p, t, box)

@@ -1,0 +1,88 @@
+"""GPU parity of the fusion configurations (Section 3.4, Table "Configurable
+fusion"): the single kernel that recomputes the encoder in its second pass
+(the paper's mega-fusion) and the three-kernel split with G_i and dE/dG_i in
+HBM (the paper's partial fusion), against the oracle and against the default
+cached configuration."""
+import dataclasses
+
+import numpy as np
+import pytest
+
+import synth
+from oracle.model import Model, evaluate
+from oracle.neighbors import neighbor_list
+from tests.gpu_helpers import gpu_eval, max_abs, log
+
+pytestmark = pytest.mark.gpu
+
+TOL64 = 1e-9
+REL32 = 1e-4
+
+
+def _eval(hp, w, fusion):
+    return gpu_eval(hp, w.weights, w.pos, w.types, w.box, fusion=fusion)
+
+
+def _rel(a, ref):
+    return max_abs(a, ref) / max(float(np.max(np.abs(ref))), 1e-300)
+
+
+@pytest.mark.parametrize("fusion", [1, 2])
+@pytest.mark.parametrize("precision", [64, 32])
+@pytest.mark.parametrize("name,n,over", [("fcc-binary-4", None, {}), ("fcc-hea6-128", 5, {}),
+                                         ("fcc-binary-4", None, {"lmax": 1, "enc_cond": 0, "reg_cond": 0}),
+                                         ("bcc-unary-32", 6, {"enc_hidden": 2, "reg_hidden": 3})])
+def test_fusion_configurations_match_oracle(fusion, precision, name, n, over):
+    w = synth.make_workload(name, seed=13, n=n, hp_overrides=dict(over, precision=precision))
+    label = f"{name}/{over}/fusion={fusion}/fp{precision}"
+    log(f"[fusion] {label}: N={len(w.pos)}")
+    g = _eval(w.hp, w, fusion)
+    m = Model(w.hp, w.weights)
+    off, idx = neighbor_list(w.pos, w.box, m.rc + m.skin)
+    ref = evaluate(m, w.pos, w.types, w.box, off, idx)
+    if precision == 64:
+        eE, eF, eV = max_abs(g["E_i"], ref["E_i"]), max_abs(g["F"], ref["F"]), max_abs(g["virial"], ref["virial"])
+        log(f"[fusion] {label}: max|dE|={eE:.2e} max|dF|={eF:.2e} max|dW|={eV:.2e}")
+        assert max(eE, eF, eV) <= TOL64
+        assert abs(g["totals"][0] - ref["E"]) <= TOL64 * len(w.pos)
+        assert max_abs(g["totals"][1:], ref["W"]) <= TOL64 * len(w.pos)
+    else:
+        eE, eF, eV = _rel(g["E_i"], ref["E_i"]), _rel(g["F"], ref["F"]), _rel(g["virial"], ref["virial"])
+        log(f"[fusion] {label}: rel dE={eE:.2e} dF={eF:.2e} dW={eV:.2e}")
+        assert max(eE, eF, eV) <= REL32
+    st = g["stats"]
+    assert st["n_listed_pairs"] == len(idx)
+    g["pot"].close()
+
+
+def test_configurations_agree_and_partial_holds_descriptor_memory():
+    """The three configurations on one input agree to rounding; the
+    three-kernel one holds (l_max + 1) k doubles per atom more."""
+    w = synth.make_workload("fcc-hea6-128", seed=3, n=6)
+    out = {}
+    for fusion in (0, 1, 2):
+        out[fusion] = _eval(w.hp, w, fusion)
+    for fusion in (1, 2):
+        for key in ("E_i", "F", "virial"):
+            d = max_abs(out[fusion][key], out[0][key])
+            log(f"[fusion] {fusion} vs cached {key}: {d:.2e}")
+            assert d <= TOL64
+    extra = out[2]["pot"].memory_bytes() - out[0]["pot"].memory_bytes()
+    assert extra == len(w.pos) * (w.hp.lmax + 1) * w.hp.k * 8
+    for g in out.values():
+        g["pot"].close()
+
+
+def test_fusion_argument_checks():
+    from paper_2608_16329_amd import Potential, MlipError
+    hp = synth.HParams(n_species=2)
+    pot = Potential(hp, synth.random_weights(hp, 0))
+    with pytest.raises(MlipError, match="ARG"):
+        pot.set_fusion(7)
+    pot.close()
+    hp16 = dataclasses.replace(hp, k=16)
+    pot = Potential(hp16, synth.random_weights(hp16, 0))
+    with pytest.raises(MlipError, match="ARG"):
+        pot.set_fusion(2)
+    pot.set_fusion(0)
+    pot.close()
