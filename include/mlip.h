@@ -70,9 +70,11 @@ typedef struct {
   double  cutoff;      /* r_c in A                                               */
   double  skin;        /* Verlet skin in A; neighbour lists use r_c + skin       */
   int32_t k;           /* radial feature width (GPU path: 16, 32 or 64)          */
-  int32_t lmax;        /* maximum angular order (GPU path: 0..3)                 */
-  int32_t angular;     /* 0 irreducible harmonic basis, d = (lmax+1)^2
-                          (1 = Cartesian monomials; not on the GPU path)         */
+  int32_t lmax;        /* maximum angular order (GPU path: 0..5 irreducible,
+                          0..3 Cartesian; above 3 and Cartesian need k = 32)     */
+  int32_t angular;     /* 0 irreducible harmonic basis, d = (lmax+1)^2;
+                          1 Cartesian monomials, d = (lmax+1)(lmax+2)(lmax+3)/6,
+                          descriptor metric l!/(a!b!c!) (Section 3.3)            */
   int32_t enc_cond;    /* encoder tables: 2 per (s_i,s_j), 1 per s_j, 0 one      */
   int32_t reg_cond;    /* head tables: 1 per s_i, 0 one                          */
   int32_t enc_width;   /* encoder hidden width (GPU path: 128)                   */

@@ -10,10 +10,14 @@
 // product.  Any two valid Q_l differ by an orthogonal factor, which leaves
 // the descriptor's squared norms unchanged; the l = 0 row is fixed to +1.
 //
-// The output table has one row per angular feature (l-major, (lmax+1)^2 <=
-// 16 rows) and one column per monomial of degree <= 3, in the order
-//   1 | x y z | x2 xy xz y2 yz z2 | x3 x2y x2z xy2 xyz xz2 y3 y2z yz2 z3
-// so feature m of direction u is sum_q table[m][q] * monomial_q(u).
+// The output table has one row per angular feature (l-major) and one column
+// per Cartesian monomial, degree by degree and lexicographic with x first
+// within a degree,
+//   1 | x y z | x2 xy xz y2 yz z2 | x3 x2y x2z xy2 xyz xz2 y3 y2z yz2 z3 | ...
+// so feature m of direction u is sum_q table[m][q] * monomial_q(u); it is
+// followed by one weight per row, the diagonal of the block metric C_l of
+// the descriptor (Eq. 5): 1 for the irreducible basis, the multinomial
+// coefficients for the Cartesian basis (whose rows are the monomials).
 #include <cmath>
 #include <string>
 #include <vector>
@@ -125,22 +129,40 @@ bool harmonic_rows(int l, std::vector<std::vector<double>>* rows, std::string* e
 
 }  // namespace
 
-bool build_angular_table(int lmax, double out[kAngRows * kMonomials], std::string* err) {
-  for (int i = 0; i < kAngRows * kMonomials; ++i) out[i] = 0.0;
-  if (lmax < 0 || lmax > 3) {
-    *err = "lmax outside 0..3 on the GPU path";
+bool build_angular_table(int lmax, int angular, int rows, int cols, std::vector<double>* out, int lrow[8],
+                         std::string* err) {
+  const int ncols_needed = (lmax + 1) * (lmax + 2) * (lmax + 3) / 6;  // monomials of degree <= lmax
+  const int nrows_needed = angular == 0 ? (lmax + 1) * (lmax + 1) : ncols_needed;
+  if (lmax < 0 || lmax > 5 || ncols_needed > cols || nrows_needed > rows || (angular != 0 && angular != 1)) {
+    *err = "angular basis does not fit the kernel's table";
     return false;
   }
+  out->assign(size_t(rows) * cols + rows, 0.0);
+  double* w = out->data() + size_t(rows) * cols;  // per-row descriptor weights
   int row = 0, col0 = 0;
   for (int l = 0; l <= lmax; ++l) {
-    std::vector<std::vector<double>> q;
-    if (!harmonic_rows(l, &q, err)) return false;
-    for (const auto& v : q) {
-      for (size_t c = 0; c < v.size(); ++c) out[row * kMonomials + col0 + int(c)] = v[c];
-      ++row;
+    lrow[l] = row;
+    const std::vector<Exp3> ex = exponents(l);
+    if (angular == 0) {
+      std::vector<std::vector<double>> q;
+      if (!harmonic_rows(l, &q, err)) return false;
+      for (const auto& v : q) {
+        for (size_t c = 0; c < v.size(); ++c) (*out)[size_t(row) * cols + col0 + int(c)] = v[c];
+        w[row] = 1.0;
+        ++row;
+      }
+    } else {
+      // Cartesian basis: the monomials themselves, with the multinomial
+      // coefficients l!/(a!b!c!) as the metric of the block
+      for (size_t c = 0; c < ex.size(); ++c) {
+        (*out)[size_t(row) * cols + col0 + int(c)] = 1.0;
+        w[row] = factorial(l) / (factorial(ex[c].a) * factorial(ex[c].b) * factorial(ex[c].c));
+        ++row;
+      }
     }
-    col0 += (l + 1) * (l + 2) / 2;
+    col0 += int(ex.size());
   }
+  for (int l = lmax + 1; l < 8; ++l) lrow[l] = row;
   return true;
 }
 

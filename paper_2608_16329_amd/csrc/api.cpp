@@ -75,8 +75,10 @@ bool structurally_valid(const mlip_hparams* hp) {
 
 bool gpu_supported(const mlip_hparams* hp, std::string* why) {
   if (hp->precision != 64 && hp->precision != 32) return *why = "precision must be 64 or 32", false;
-  if (hp->angular != 0) return *why = "only the irreducible angular basis runs on the GPU path", false;
-  if (hp->lmax < 0 || hp->lmax > 3) return *why = "lmax must be in 0..3 on the GPU path", false;
+  if (hp->angular == 0 && (hp->lmax < 0 || hp->lmax > 5)) return *why = "lmax must be in 0..5 (irreducible)", false;
+  if (hp->angular == 1 && (hp->lmax < 0 || hp->lmax > 3)) return *why = "lmax must be in 0..3 (Cartesian)", false;
+  if (angular_config(hp->angular, hp->lmax) != 0 && hp->k != 32)
+    return *why = "the Cartesian basis and l_max > 3 run with k = 32 only", false;
   if (hp->k != 16 && hp->k != 32 && hp->k != 64) return *why = "k must be 16, 32 or 64 on the GPU path", false;
   if (hp->enc_width != kEncWidth) return *why = "enc_width must be 128 on the GPU path", false;
   if (hp->reg_width != kHeadWidth) return *why = "reg_width must be 64 on the GPU path", false;
@@ -218,9 +220,13 @@ mlip_status mlip_create(const mlip_hparams* hp, const double* weights_host, size
     }
     head.insert(head.end(), p, p + R + 1);
   }
-  double qc[kAngRows * kMonomials];
+  ctx->acfg = angular_config(hp->angular, hp->lmax);
+  int qrows = 0, qcols = 0;
+  angular_table_shape(ctx->acfg, &qrows, &qcols);
+  std::vector<double> qc;
   std::string err;
-  if (!build_angular_table(hp->lmax, qc, &err) || enc.size() != ctx->enc_stride * ctx->n_enc ||
+  if (!build_angular_table(hp->lmax, hp->angular, qrows, qcols, &qc, ctx->lrow, &err) ||
+      enc.size() != ctx->enc_stride * ctx->n_enc ||
       head.size() != ctx->head_stride * ctx->n_head) {
     delete ctx;
     return MLIP_E_ARG;
@@ -230,7 +236,7 @@ mlip_status mlip_create(const mlip_hparams* hp, const double* weights_host, size
   const size_t eb = ctx->elem_bytes;
   if ((st = ensure(ctx, &ctx->d_enc, &cap, enc.size() * eb, "encoder")) != MLIP_OK ||
       (st = ensure(ctx, &ctx->d_head, &cap2, head.size() * eb, "head")) != MLIP_OK ||
-      (st = ensure(ctx, &ctx->d_qc, &cap3, size_t(kAngRows * kMonomials) * eb, "tables")) != MLIP_OK ||
+      (st = ensure(ctx, &ctx->d_qc, &cap3, qc.size() * eb, "tables")) != MLIP_OK ||
       (st = ensure(ctx, &ctx->d_totals, &cap4, size_t(16), "totals")) != MLIP_OK ||
       (st = ensure(ctx, &ctx->d_counters, &cap5, size_t(4), "counters")) != MLIP_OK ||
       (st = ensure(ctx, &ctx->d_flags, &cap6, size_t(4), "flags")) != MLIP_OK ||
@@ -241,7 +247,7 @@ mlip_status mlip_create(const mlip_hparams* hp, const double* weights_host, size
   }
   if (upload(ctx->d_enc, enc.data(), enc.size(), eb) != hipSuccess ||
       upload(ctx->d_head, head.data(), head.size(), eb) != hipSuccess ||
-      upload(ctx->d_qc, qc, size_t(kAngRows * kMonomials), eb) != hipSuccess) {
+      upload(ctx->d_qc, qc.data(), qc.size(), eb) != hipSuccess) {
     (void)hipGetLastError();
     mlip_destroy(ctx);
     return MLIP_E_HIP;
@@ -344,7 +350,7 @@ mlip_status mlip_build_neighbors(mlip_ctx* ctx, int64_t n_atoms, const double* p
   ctx->max_row = flags[1];
 
   // fused-kernel tiling and workspace
-  const int T = std::max(1, std::min(fused_tile_max(ctx->hp.k, ctx->hp.precision), kEntCap / std::max(1, ctx->max_row)));
+  const int T = std::max(1, std::min(fused_tile_max(ctx->hp.k, ctx->hp.precision, ctx->acfg), kEntCap / std::max(1, ctx->max_row)));
   ctx->tile_atoms = T;
   int64_t tiles = 0;
   for (int sp_i = 0; sp_i < C; ++sp_i) tiles += (int64_t(sp[sp_i + 1] - sp[sp_i]) + T - 1) / T;
@@ -380,6 +386,7 @@ mlip_status mlip_compute(mlip_ctx* ctx, const double* pos_dev, double* energy_de
   a.enc = ctx->d_enc;
   a.head = ctx->d_head;
   a.qc = ctx->d_qc;
+  for (int l = 0; l < 8; ++l) a.lrow[l] = ctx->lrow[l];
   a.energy = energy_dev;
   a.forces = forces_dev;
   a.virial = virial_dev;
@@ -417,11 +424,11 @@ mlip_status mlip_compute(mlip_ctx* ctx, const double* pos_dev, double* energy_de
   if (ctx->n_tiles > 0) {
     const int k = ctx->hp.k, prec = ctx->hp.precision;
     if (ctx->fusion == MLIP_FUSION_PARTIAL) {
-      MLIP_HIP(ctx, launch_fused(k, prec, 2, a, ctx->n_blocks, s));
-      MLIP_HIP(ctx, launch_fused(k, prec, 3, a, ctx->n_blocks, s));
-      MLIP_HIP(ctx, launch_fused(k, prec, 4, a, ctx->n_blocks, s));
+      MLIP_HIP(ctx, launch_fused(k, prec, ctx->acfg, 2, a, ctx->n_blocks, s));
+      MLIP_HIP(ctx, launch_fused(k, prec, ctx->acfg, 3, a, ctx->n_blocks, s));
+      MLIP_HIP(ctx, launch_fused(k, prec, ctx->acfg, 4, a, ctx->n_blocks, s));
     } else {
-      MLIP_HIP(ctx, launch_fused(k, prec, ctx->fusion == MLIP_FUSION_RECOMPUTE ? 1 : 0, a, ctx->n_blocks, s));
+      MLIP_HIP(ctx, launch_fused(k, prec, ctx->acfg, ctx->fusion == MLIP_FUSION_RECOMPUTE ? 1 : 0, a, ctx->n_blocks, s));
     }
   }
   if (totals_host) {
@@ -460,8 +467,10 @@ mlip_status mlip_set_fusion(mlip_ctx* ctx, int32_t fusion) {
   ctx->err.clear();
   if (fusion != MLIP_FUSION_CACHED && fusion != MLIP_FUSION_RECOMPUTE && fusion != MLIP_FUSION_PARTIAL)
     return fail(ctx, MLIP_E_ARG, "unknown fusion configuration");
-  if (fusion != MLIP_FUSION_CACHED && ctx->hp.k != 32)
-    return fail(ctx, MLIP_E_ARG, "the recompute and three-kernel configurations exist for k = 32 only");
+  if (fusion != MLIP_FUSION_CACHED && (ctx->hp.k != 32 || ctx->acfg != 0))
+    return fail(ctx, MLIP_E_ARG,
+                "the recompute and three-kernel configurations exist for k = 32 and the irreducible basis "
+                "with l_max <= 3 only");
   ctx->fusion = fusion;
   return MLIP_OK;
 }

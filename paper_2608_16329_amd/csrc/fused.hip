@@ -173,20 +173,69 @@ __device__ __forceinline__ void monomial_grads(R x, R y, R z, R gx[kMonomials], 
   gx[19] = 0; gy[19] = 0; gz[19] = 3 * zz;
 }
 
-template <int K, int TM, typename R, int NW>
+// Exponents (a, b, c) of the Cartesian monomials of degree <= 5, degree by
+// degree and lexicographic with x first within a degree (the column order of
+// the angular table; its first 20 entries are the order above).
+struct MonoExp {
+  unsigned char e[56][3];
+  constexpr MonoExp() : e{} {
+    int i = 0;
+    for (int d = 0; d <= 5; ++d)
+      for (int a = d; a >= 0; --a)
+        for (int b = d - a; b >= 0; --b) {
+          e[i][0] = (unsigned char)a;
+          e[i][1] = (unsigned char)b;
+          e[i][2] = (unsigned char)(d - a - b);
+          ++i;
+        }
+  }
+};
+constexpr MonoExp kMonoExp{};
+
+// The NM monomials (20: degree <= 3, 56: degree <= 5) of (x, y, z) and, when
+// kGrad, their gradients.
+template <int NM, bool kGrad, typename R>
+__device__ __forceinline__ void monomials_n(R x, R y, R z, R m[NM], R gx[NM], R gy[NM], R gz[NM]) {
+  if constexpr (NM == kMonomials) {
+    monomials(x, y, z, m);
+    if (kGrad) monomial_grads(x, y, z, gx, gy, gz);
+  } else {
+    R px[6], py[6], pz[6];
+    px[0] = py[0] = pz[0] = R(1);
+#pragma unroll
+    for (int k = 1; k < 6; ++k) {
+      px[k] = px[k - 1] * x;
+      py[k] = py[k - 1] * y;
+      pz[k] = pz[k - 1] * z;
+    }
+#pragma unroll
+    for (int i = 0; i < NM; ++i) {
+      const int a = kMonoExp.e[i][0], b = kMonoExp.e[i][1], c = kMonoExp.e[i][2];
+      m[i] = px[a] * py[b] * pz[c];
+      if (kGrad) {
+        gx[i] = a ? R(a) * px[a > 0 ? a - 1 : 0] * py[b] * pz[c] : R(0);
+        gy[i] = b ? R(b) * px[a] * py[b > 0 ? b - 1 : 0] * pz[c] : R(0);
+        gz[i] = c ? R(c) * px[a] * py[b] * pz[c > 0 ? c - 1 : 0] : R(0);
+      }
+    }
+  }
+}
+
+template <int K, int TM, typename R, int NW, int DR, int NM>
 struct Smem {
-  R P[TM][kAngRows][K + 1];  // moment, then its adjoint W (padded rows)
+  R P[TM][DR][K + 1];  // moment, then its adjoint W (padded rows)
   // Pass 1 reads the first-layer weights; the head runs after pass 1 and
   // before the next tile is staged, so its activations reuse those bytes.
   union {
     R l0[kMaxSpecies][2][kEncWidth];  // w0, b0 of the tile's encoder tables, by neighbour species
     struct {
-      R xT[4 * K][16];              // head input vec(G), feature-major
+      R xT[(NM == 20 ? 4 : 6) * K][16];  // head input vec(G), feature-major
       R yT[kHeadWidth][16];         // head activations
       R gT[kHeadWidth][16];         // head backward scratch
     } hd;
   } u;
-  R qc[kAngRows][kMonomials];
+  R qc[DR][NM];        // angular features over the monomials
+  R rw[DR];            // descriptor weight of each angular row (metric C_l)
   double tpos[TM][3];
   double Fi[TM][3];
   double Wi[TM][9];
@@ -215,8 +264,8 @@ struct PairPos {
   double x, y, z;
 };
 
-template <int K, int TM, typename R, int NW>
-__device__ __forceinline__ PairPos load_pair_pos(const FusedArgs& A, const Smem<K, TM, R, NW>& S, int ch) {
+template <int K, int TM, typename R, int NW, int DR, int NM>
+__device__ __forceinline__ PairPos load_pair_pos(const FusedArgs& A, const Smem<K, TM, R, NW, DR, NM>& S, int ch) {
   const int c = threadIdx.x & 15;
   PairPos p{0.0, 0.0, 0.0};
   if (c < S.ch_count[ch]) {
@@ -245,8 +294,8 @@ struct Stream {
 
 // Distance of the pair in column c of chunk ch (Eq. 1), in float64; 1 for
 // the padding columns of a partial chunk.
-template <int K, int TM, typename R, int NW>
-__device__ __forceinline__ double pair_distance(const FusedArgs& A, const Smem<K, TM, R, NW>& S, int ch,
+template <int K, int TM, typename R, int NW, int DR, int NM>
+__device__ __forceinline__ double pair_distance(const FusedArgs& A, const Smem<K, TM, R, NW, DR, NM>& S, int ch,
                                                 const PairPos& pp, double* ux, double* uy, double* uz, int* atom) {
   const int c = threadIdx.x & 15;
   *ux = 1.0; *uy = 0.0; *uz = 0.0; *atom = -1;
@@ -263,8 +312,8 @@ __device__ __forceinline__ double pair_distance(const FusedArgs& A, const Smem<K
 }
 
 // Encoder table of chunk ch (pair conditioning, Section 3.2).
-template <int K, int TM, typename R, int NW>
-__device__ __forceinline__ const R* chunk_table(const FusedArgs& A, const Smem<K, TM, R, NW>& S, int ch) {
+template <int K, int TM, typename R, int NW, int DR, int NM>
+__device__ __forceinline__ const R* chunk_table(const FusedArgs& A, const Smem<K, TM, R, NW, DR, NM>& S, int ch) {
   const int sj = S.ch_s[ch], si = S.tile_species;
   const int tau = A.enc_cond == 2 ? si * A.C + sj : (A.enc_cond == 1 ? sj : 0);
   return static_cast<const R*>(A.enc) + (long long)tau * A.enc_stride;
@@ -276,8 +325,8 @@ __device__ __forceinline__ const R* chunk_table(const FusedArgs& A, const Smem<K
 // 8 x 32 MFMA steps whose forward and tangent columns share each weight
 // fragment.  On return h[T][i], dh[T][i] hold rows 16T + drow(i, g) of
 // column c; the result is the output-layer section of the table.
-template <int K, int TM, typename R, int NW>
-__device__ __forceinline__ const R* encoder_hidden(const FusedArgs& A, const Smem<K, TM, R, NW>& S, int sj, R r,
+template <int K, int TM, typename R, int NW, int DR, int NM>
+__device__ __forceinline__ const R* encoder_hidden(const FusedArgs& A, const Smem<K, TM, R, NW, DR, NM>& S, int sj, R r,
                                                    const R* __restrict__ tab, R (&h)[8][4], R (&dh)[8][4]) {
   typedef Stream<K, R> St;
   typedef typename St::vh_t vh_t;
@@ -442,8 +491,8 @@ __device__ __forceinline__ void encoder_out_cols(const R* __restrict__ layer, co
 
 // Pass 1 on one chunk: encoder forward + tangent, moment accumulation and,
 // when kWs, the workspace write of (m, dm).
-template <int K, int TM, typename R, int NW, bool kWs>
-__device__ void pass1_chunk(const FusedArgs& A, Smem<K, TM, R, NW>& S, int ch, const PairPos pp, R* __restrict__ wsc) {
+template <int K, int TM, typename R, int NW, int DR, int NM, bool kWs>
+__device__ void pass1_chunk(const FusedArgs& A, Smem<K, TM, R, NW, DR, NM>& S, int ch, const PairPos pp, R* __restrict__ wsc) {
   constexpr int KT = K / 16;
   const int lane = threadIdx.x & 63, g = lane >> 4, c = lane & 15;
   const int start = S.ch_start[ch], count = S.ch_count[ch];
@@ -460,9 +509,11 @@ __device__ void pass1_chunk(const FusedArgs& A, Smem<K, TM, R, NW>& S, int ch, c
   encoder_out_rows<K, R>(layer, h, dh, mo, dmo);
 
   // moment: P[mm][col] += sum_pairs fc * a_mm(u) * m[pair][col], one MFMA
-  // product per centre atom present in the chunk (pairs of other atoms are
-  // masked to zero in the A operand)
-  R av[4];
+  // product per centre atom present in the chunk and 16-row tile of the
+  // angular features (pairs of other atoms are masked to zero in the A
+  // operand)
+  constexpr int NA = DR / 16;
+  R av[NA][4];
   int aa[4];
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
@@ -470,28 +521,34 @@ __device__ void pass1_chunk(const FusedArgs& A, Smem<K, TM, R, NW>& S, int ch, c
     const R px = __shfl(ux, src, 64), py = __shfl(uy, src, 64), pz = __shfl(uz, src, 64);
     const R pf = __shfl(fc, src, 64);
     aa[q] = __shfl(atom, src, 64);
-    R mono[kMonomials];
-    monomials(px, py, pz, mono);
-    R s = 0;
+    R mono[NM];
+    monomials_n<NM, false>(px, py, pz, mono, mono, mono, mono);
 #pragma unroll
-    for (int m = 0; m < kMonomials; ++m) s += S.qc[c][m] * mono[m];
-    av[q] = pf * s;
+    for (int ta = 0; ta < NA; ++ta) {
+      R s = 0;
+#pragma unroll
+      for (int m = 0; m < NM; ++m) s += S.qc[16 * ta + c][m] * mono[m];
+      av[ta][q] = pf * s;
+    }
   }
   const int a_first = S.pair_a[start], a_last = S.pair_a[start + count - 1];
   for (int a = a_first; a <= a_last; ++a) {
-    v4<R> pacc[KT];
 #pragma unroll
-    for (int Tc = 0; Tc < KT; ++Tc) pacc[Tc] = v4<R>{0, 0, 0, 0};
+    for (int ta = 0; ta < NA; ++ta) {
+      v4<R> pacc[KT];
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const R av_a = aa[q] == a ? av[q] : R(0);
+      for (int Tc = 0; Tc < KT; ++Tc) pacc[Tc] = v4<R>{0, 0, 0, 0};
 #pragma unroll
-      for (int Tc = 0; Tc < KT; ++Tc) pacc[Tc] = mfma(av_a, mo[Tc][q], pacc[Tc]);
+      for (int q = 0; q < 4; ++q) {
+        const R av_a = aa[q] == a ? av[ta][q] : R(0);
+#pragma unroll
+        for (int Tc = 0; Tc < KT; ++Tc) pacc[Tc] = mfma(av_a, mo[Tc][q], pacc[Tc]);
+      }
+#pragma unroll
+      for (int Tc = 0; Tc < KT; ++Tc)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) atomicAdd(&S.P[a][16 * ta + drow<R>(q, g)][16 * Tc + c], pacc[Tc][q]);
     }
-#pragma unroll
-    for (int Tc = 0; Tc < KT; ++Tc)
-#pragma unroll
-      for (int q = 0; q < 4; ++q) atomicAdd(&S.P[a][drow<R>(q, g)][16 * Tc + c], pacc[Tc][q]);
   }
 
   if (kWs) {
@@ -517,8 +574,8 @@ struct Pass2In {
   PairPos pp;
 };
 
-template <int K, int TM, typename R, int NW>
-__device__ __forceinline__ void pass2_load(const FusedArgs& A, const Smem<K, TM, R, NW>& S, int ch,
+template <int K, int TM, typename R, int NW, int DR, int NM>
+__device__ __forceinline__ void pass2_load(const FusedArgs& A, const Smem<K, TM, R, NW, DR, NM>& S, int ch,
                                            const R* __restrict__ wsc, Pass2In<K, R>& in) {
   constexpr int VW = 16 / int(sizeof(R));
   constexpr int NV = K / 4 / VW;  // 16-byte loads per lane for m (and for dm)
@@ -544,8 +601,8 @@ __device__ __forceinline__ void pass2_load(const FusedArgs& A, const Smem<K, TM,
 
 // Inputs of pass 2 for one chunk by recomputing the encoder instead of
 // reading the workspace (the paper's mega-fusion, Section 3.4).
-template <int K, int TM, typename R, int NW>
-__device__ __forceinline__ void pass2_recompute(const FusedArgs& A, const Smem<K, TM, R, NW>& S, int ch,
+template <int K, int TM, typename R, int NW, int DR, int NM>
+__device__ __forceinline__ void pass2_recompute(const FusedArgs& A, const Smem<K, TM, R, NW, DR, NM>& S, int ch,
                                                 const PairPos& pp, Pass2In<K, R>& in) {
   double ux, uy, uz;
   int atom;
@@ -557,8 +614,8 @@ __device__ __forceinline__ void pass2_recompute(const FusedArgs& A, const Smem<K
 }
 
 // Pass 2 on one chunk: W contractions, partial forces and scatter.
-template <int K, int TM, typename R, int NW>
-__device__ void pass2_chunk(const FusedArgs& A, Smem<K, TM, R, NW>& S, int ch, const Pass2In<K, R>& in) {
+template <int K, int TM, typename R, int NW, int DR, int NM>
+__device__ void pass2_chunk(const FusedArgs& A, Smem<K, TM, R, NW, DR, NM>& S, int ch, const Pass2In<K, R>& in) {
   constexpr int KT = K / 16;
   const int lane = threadIdx.x & 63, g = lane >> 4, c = lane & 15;
   const int start = S.ch_start[ch], count = S.ch_count[ch];
@@ -581,49 +638,58 @@ __device__ void pass2_chunk(const FusedArgs& A, Smem<K, TM, R, NW>& S, int ch, c
   const R fc = valid ? R(0.5 * (1.0 + cos(arg))) : R(0);
   const R dfc = valid ? R(-0.5 * M_PI / A.rc * sin(arg)) : R(0);
 
-  // (W m) and (W dm) for this column's own centre atom
-  v4<R> wm = v4<R>{0, 0, 0, 0}, wdm = v4<R>{0, 0, 0, 0};
+  // (W m) and (W dm) for this column's own centre atom, one 16-row tile of
+  // the angular features at a time
+  constexpr int NA = DR / 16;
+  v4<R> wm[NA], wdm[NA];
+#pragma unroll
+  for (int ta = 0; ta < NA; ++ta) wm[ta] = wdm[ta] = v4<R>{0, 0, 0, 0};
   const int a_first = S.pair_a[start], a_last = S.pair_a[start + count - 1];
   for (int a = a_first; a <= a_last; ++a) {
-    v4<R> t1 = v4<R>{0, 0, 0, 0}, t2 = v4<R>{0, 0, 0, 0};
 #pragma unroll
-    for (int Tc = 0; Tc < KT; ++Tc)
+    for (int ta = 0; ta < NA; ++ta) {
+      v4<R> t1 = v4<R>{0, 0, 0, 0}, t2 = v4<R>{0, 0, 0, 0};
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const R w = S.P[a][c][16 * Tc + drow<R>(i, g)];
-        t1 = mfma(w, in.mB[Tc][i], t1);
-        t2 = mfma(w, in.dmB[Tc][i], t2);
+      for (int Tc = 0; Tc < KT; ++Tc)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const R w = S.P[a][16 * ta + c][16 * Tc + drow<R>(i, g)];
+          t1 = mfma(w, in.mB[Tc][i], t1);
+          t2 = mfma(w, in.dmB[Tc][i], t2);
+        }
+      if (atom == a) {
+        wm[ta] = t1;
+        wdm[ta] = t2;
       }
-    if (atom == a) {
-      wm = t1;
-      wdm = t2;
     }
   }
 
-  // angular features a_mm and gradients for rows mm = drow(q, g) of this pair
-  R mono[kMonomials], gx[kMonomials], gy[kMonomials], gz[kMonomials];
-  monomials(R(ux), R(uy), R(uz), mono);
-  monomial_grads(R(ux), R(uy), R(uz), gx, gy, gz);
+  // angular features a_mm and gradients for rows mm = 16 ta + drow(q, g) of
+  // this pair
+  R mono[NM], gx[NM], gy[NM], gz[NM];
+  monomials_n<NM, true>(R(ux), R(uy), R(uz), mono, gx, gy, gz);
   R s = 0, tx = 0, ty = 0, tz = 0;
 #pragma unroll
-  for (int q = 0; q < 4; ++q) {
-    const int mm = drow<R>(q, g);
-    R a_v = 0, a_x = 0, a_y = 0, a_z = 0;
+  for (int ta = 0; ta < NA; ++ta)
 #pragma unroll
-    for (int m = 0; m < kMonomials; ++m) {
-      const R co = S.qc[mm][m];
-      a_v += co * mono[m];
-      a_x += co * gx[m];
-      a_y += co * gy[m];
-      a_z += co * gz[m];
+    for (int q = 0; q < 4; ++q) {
+      const int mm = 16 * ta + drow<R>(q, g);
+      R a_v = 0, a_x = 0, a_y = 0, a_z = 0;
+#pragma unroll
+      for (int m = 0; m < NM; ++m) {
+        const R co = S.qc[mm][m];
+        a_v += co * mono[m];
+        a_x += co * gx[m];
+        a_y += co * gy[m];
+        a_z += co * gz[m];
+      }
+      const R v = fc * wm[ta][q];                       // v = W g
+      const R wg = dfc * wm[ta][q] + fc * wdm[ta][q];   // W g'
+      s += a_v * wg;
+      tx += a_x * v;
+      ty += a_y * v;
+      tz += a_z * v;
     }
-    const R v = fc * wm[q];                   // v = W g
-    const R wg = dfc * wm[q] + fc * wdm[q];   // W g'
-    s += a_v * wg;
-    tx += a_x * v;
-    ty += a_y * v;
-    tz += a_z * v;
-  }
 #pragma unroll
   for (int o = 16; o <= 32; o <<= 1) {
     s += __shfl_xor(s, o, 64);
@@ -662,25 +728,29 @@ __device__ void pass2_chunk(const FusedArgs& A, Smem<K, TM, R, NW>& S, int ch, c
 }
 
 // Descriptor value x[in] = vec(G)[in] of tile atom a (Eq. 5): the l = 0
-// block is linear, blocks l >= 1 are squared norms over their 2l + 1 rows.
-template <int K, int TM, typename R, int NW>
-__device__ __forceinline__ R descriptor_value(const Smem<K, TM, R, NW>& S, int a, int in) {
+// block is linear, a block l >= 1 (angular rows lrow[l] .. lrow[l+1]-1) is
+// the quadratic form sum_m rw[m] P[m][col]^2 with the block's diagonal
+// metric (1 for the irreducible basis, the multinomial coefficients for the
+// Cartesian one).
+template <int K, int TM, typename R, int NW, int DR, int NM>
+__device__ __forceinline__ R descriptor_value(const FusedArgs& A, const Smem<K, TM, R, NW, DR, NM>& S, int a, int in) {
   const int l = in / K, col = in % K;
   if (l == 0) return S.P[a][0][col];
   R v = 0;
-  for (int mm = l * l; mm < (l + 1) * (l + 1); ++mm) v += S.P[a][mm][col] * S.P[a][mm][col];
+  for (int mm = A.lrow[l]; mm < A.lrow[l + 1]; ++mm) v += S.rw[mm] * S.P[a][mm][col] * S.P[a][mm][col];
   return v;
 }
 
 // W = dE/dP (Eq. 7) for tile atom a from dE/dx[in]: W[0][col] = dE/dG[0][col],
-// W[m][col] = 2 dE/dG[l][col] P[m][col]; overwrites P.
-template <int K, int TM, typename R, int NW>
-__device__ __forceinline__ void adjoint_from_grad(Smem<K, TM, R, NW>& S, int a, int in, R d) {
+// W[m][col] = 2 dE/dG[l][col] rw[m] P[m][col]; overwrites P.
+template <int K, int TM, typename R, int NW, int DR, int NM>
+__device__ __forceinline__ void adjoint_from_grad(const FusedArgs& A, Smem<K, TM, R, NW, DR, NM>& S, int a, int in,
+                                                  R d) {
   const int l = in / K, col = in % K;
   if (l == 0) {
     S.P[a][0][col] = d;
   } else {
-    for (int mm = l * l; mm < (l + 1) * (l + 1); ++mm) S.P[a][mm][col] *= R(2) * d;
+    for (int mm = A.lrow[l]; mm < A.lrow[l + 1]; ++mm) S.P[a][mm][col] *= R(2) * S.rw[mm] * d;
   }
 }
 
@@ -692,8 +762,8 @@ __device__ __forceinline__ void adjoint_from_grad(Smem<K, TM, R, NW>& S, int a, 
 // pass.  With kRegress (the regression kernel of the three-kernel
 // configuration) the descriptor comes from HBM and dE/dx goes back to HBM in
 // its place instead of forming W.
-template <int K, int TM, typename R, int NW, bool kRegress>
-__device__ void head_stage(const FusedArgs& A, Smem<K, TM, R, NW>& S) {
+template <int K, int TM, typename R, int NW, int DR, int NM, bool kRegress>
+__device__ void head_stage(const FusedArgs& A, Smem<K, TM, R, NW, DR, NM>& S) {
   constexpr int RW = kHeadWidth;
   constexpr int HS = 2 * RW * RW + RW;  // one hidden layer: A_t and A_t^T fragments, c_t
   const int tid = threadIdx.x, lane = tid & 63, g = lane >> 4, c = lane & 15, w = tid >> 6;
@@ -704,7 +774,7 @@ __device__ void head_stage(const FusedArgs& A, Smem<K, TM, R, NW>& S) {
   for (int u = tid; u < 16 * nin; u += (64 * NW)) {
     const int a = u & 15, in = u >> 4;
     R v = 0;
-    if (a < na) v = kRegress ? gbuf[(long long)a * nin + in] : descriptor_value(S, a, in);
+    if (a < na) v = kRegress ? gbuf[(long long)a * nin + in] : descriptor_value(A, S, a, in);
     S.u.hd.xT[in][a] = v;
   }
   __syncthreads();
@@ -803,7 +873,7 @@ __device__ void head_stage(const FusedArgs& A, Smem<K, TM, R, NW>& S) {
         if (kRegress)
           gbuf[(long long)c * nin + in] = acc[q];
         else
-          adjoint_from_grad(S, c, in, acc[q]);
+          adjoint_from_grad(A, S, c, in, acc[q]);
       }
     }
   }
@@ -813,8 +883,8 @@ __device__ void head_stage(const FusedArgs& A, Smem<K, TM, R, NW>& S) {
 
 // First-layer weights (w0, b0) of the tile's encoder tables, one per
 // neighbour species, into LDS.
-template <int K, int TM, typename R, int NW>
-__device__ __forceinline__ void stage_first_layer(const FusedArgs& A, Smem<K, TM, R, NW>& S,
+template <int K, int TM, typename R, int NW, int DR, int NM>
+__device__ __forceinline__ void stage_first_layer(const FusedArgs& A, Smem<K, TM, R, NW, DR, NM>& S,
                                                   const R* __restrict__ enc) {
   for (int u = threadIdx.x; u < A.C * 2 * kEncWidth; u += 64 * NW) {
     const int sj = u / (2 * kEncWidth), rem = u % (2 * kEncWidth);
@@ -831,17 +901,18 @@ __device__ __forceinline__ void stage_first_layer(const FusedArgs& A, Smem<K, TM
 // E and dE/dG to HBM) and derivation (Eqs. 7-10, recomputing P).
 enum Mode { kCached = 0, kRecompute = 1, kEncode = 2, kRegress = 3, kDerive = 4 };
 
-template <int K, int TM, typename R, int NW, int MODE>
+template <int K, int TM, typename R, int NW, int DR, int NM, int MODE>
 __global__ __launch_bounds__(64 * NW, 1) void k_fused(FusedArgs A) {
   extern __shared__ __align__(16) unsigned char smem_raw[];
-  Smem<K, TM, R, NW>& S = *reinterpret_cast<Smem<K, TM, R, NW>*>(smem_raw);
+  Smem<K, TM, R, NW, DR, NM>& S = *reinterpret_cast<Smem<K, TM, R, NW, DR, NM>*>(smem_raw);
   const int tid = threadIdx.x, wave = tid >> 6;
   const long long chunk_elems = 2LL * K * 16;
   R* __restrict__ ws_slot = static_cast<R*>(A.ws) + (long long)blockIdx.x * A.ws_slot;
   const R* __restrict__ enc = static_cast<const R*>(A.enc);
   const R* __restrict__ qc = static_cast<const R*>(A.qc);
 
-  for (int u = tid; u < kAngRows * kMonomials; u += (64 * NW)) S.qc[u / kMonomials][u % kMonomials] = qc[u];
+  for (int u = tid; u < DR * NM; u += (64 * NW)) S.qc[u / NM][u % NM] = qc[u];
+  for (int u = tid; u < DR; u += 64 * NW) S.rw[u] = qc[DR * NM + u];
 
   // XCD-aware assignment: blocks are dispatched round-robin over the 8 XCDs,
   // so block b works on the b%8-th contiguous eighth of the tile list and
@@ -892,7 +963,7 @@ __global__ __launch_bounds__(64 * NW, 1) void k_fused(FusedArgs A) {
       if (tid == 0) S.row_beg[0] = A.offsets[a0];
     }
     for (int u = tid; u < kMaxSpecies * TM; u += (64 * NW)) S.cnt[u / TM][u % TM] = 0;
-    for (int u = tid; u < TM * kAngRows * (K + 1); u += (64 * NW)) (&S.P[0][0][0])[u] = R(0);
+    for (int u = tid; u < TM * DR * (K + 1); u += (64 * NW)) (&S.P[0][0][0])[u] = R(0);
     __syncthreads();
     const int nent = S.ent_base[na];
     const long long ebase = S.row_beg[0];
@@ -993,7 +1064,7 @@ __global__ __launch_bounds__(64 * NW, 1) void k_fused(FusedArgs A) {
       for (int ch = wave; ch < nch; ch += NW) {
         const PairPos cur = next;
         if (ch + NW < nch) next = load_pair_pos(A, S, ch + NW);
-        pass1_chunk<K, TM, R, NW, kWs>(A, S, ch, cur, ws_slot + ch * chunk_elems);
+        pass1_chunk<K, TM, R, NW, DR, NM, kWs>(A, S, ch, cur, ws_slot + ch * chunk_elems);
       }
     }
     __syncthreads();
@@ -1001,9 +1072,9 @@ __global__ __launch_bounds__(64 * NW, 1) void k_fused(FusedArgs A) {
 
     // ---- C: descriptor, head, W ------------------------------------------
     if constexpr (MODE == kCached || MODE == kRecompute) {
-      head_stage<K, TM, R, NW, false>(A, S);
+      head_stage<K, TM, R, NW, DR, NM, false>(A, S);
     } else if constexpr (MODE == kRegress) {
-      head_stage<K, TM, R, NW, true>(A, S);
+      head_stage<K, TM, R, NW, DR, NM, true>(A, S);
     } else {
       // encoding kernel: G to HBM; derivation kernel: W from dE/dG in HBM
       const int nin = (A.lmax + 1) * K;
@@ -1011,9 +1082,9 @@ __global__ __launch_bounds__(64 * NW, 1) void k_fused(FusedArgs A) {
       for (int u = tid; u < na * nin; u += 64 * NW) {
         const int a = u / nin, in = u % nin;
         if constexpr (MODE == kEncode)
-          gbuf[u] = descriptor_value(S, a, in);
+          gbuf[u] = descriptor_value(A, S, a, in);
         else
-          adjoint_from_grad(S, a, in, gbuf[u]);
+          adjoint_from_grad(A, S, a, in, gbuf[u]);
       }
       __syncthreads();
     }
@@ -1025,7 +1096,7 @@ __global__ __launch_bounds__(64 * NW, 1) void k_fused(FusedArgs A) {
       for (int ch = wave; ch < nch; ch += NW) {
         const Pass2In<K, R> cur = next;
         if (ch + NW < nch) pass2_load(A, S, ch + NW, ws_slot + (ch + NW) * chunk_elems, next);
-        pass2_chunk<K, TM, R, NW>(A, S, ch, cur);
+        pass2_chunk<K, TM, R, NW, DR, NM>(A, S, ch, cur);
       }
     } else if constexpr (MODE == kRecompute) {
       // the head's activations overwrote the first-layer weights in LDS
@@ -1037,7 +1108,7 @@ __global__ __launch_bounds__(64 * NW, 1) void k_fused(FusedArgs A) {
         if (ch + NW < nch) next = load_pair_pos(A, S, ch + NW);
         Pass2In<K, R> in;
         pass2_recompute(A, S, ch, cur, in);
-        pass2_chunk<K, TM, R, NW>(A, S, ch, in);
+        pass2_chunk<K, TM, R, NW, DR, NM>(A, S, ch, in);
       }
     }
     __syncthreads();
@@ -1081,55 +1152,76 @@ __global__ __launch_bounds__(64 * NW, 1) void k_fused(FusedArgs A) {
   }
 }
 
-template <int K, int TM, typename R, int NW, int MODE>
+template <int K, int TM, typename R, int NW, int DR, int NM, int MODE>
 hipError_t launch_k(const FusedArgs& a, int n_blocks, hipStream_t s) {
-  static_assert(sizeof(Smem<K, TM, R, NW>) <= 160 * 1024, "tile state exceeds the 160 KB LDS of a CU");
-  const size_t smem = sizeof(Smem<K, TM, R, NW>);
+  static_assert(sizeof(Smem<K, TM, R, NW, DR, NM>) <= 160 * 1024, "tile state exceeds the 160 KB LDS of a CU");
+  const size_t smem = sizeof(Smem<K, TM, R, NW, DR, NM>);
   static bool attr_set = false;
   if (!attr_set) {
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_fused<K, TM, R, NW, MODE>),
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_fused<K, TM, R, NW, DR, NM, MODE>),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, int(smem));
     if (e != hipSuccess) return e;
     attr_set = true;
   }
-  k_fused<K, TM, R, NW, MODE><<<dim3(unsigned(n_blocks)), dim3(64 * NW), smem, s>>>(a);
+  k_fused<K, TM, R, NW, DR, NM, MODE><<<dim3(unsigned(n_blocks)), dim3(64 * NW), smem, s>>>(a);
   return hipGetLastError();
 }
 
-template <int K, int TM, typename R, int NW>
+template <int K, int TM, typename R, int NW, int DR, int NM>
 hipError_t launch_mode(int mode, const FusedArgs& a, int n_blocks, hipStream_t s) {
   switch (mode) {
-    case kCached: return launch_k<K, TM, R, NW, kCached>(a, n_blocks, s);
-    case kRecompute: return launch_k<K, TM, R, NW, kRecompute>(a, n_blocks, s);
-    case kEncode: return launch_k<K, TM, R, NW, kEncode>(a, n_blocks, s);
-    case kRegress: return launch_k<K, TM, R, NW, kRegress>(a, n_blocks, s);
-    case kDerive: return launch_k<K, TM, R, NW, kDerive>(a, n_blocks, s);
+    case kCached: return launch_k<K, TM, R, NW, DR, NM, kCached>(a, n_blocks, s);
+    case kRecompute: return launch_k<K, TM, R, NW, DR, NM, kRecompute>(a, n_blocks, s);
+    case kEncode: return launch_k<K, TM, R, NW, DR, NM, kEncode>(a, n_blocks, s);
+    case kRegress: return launch_k<K, TM, R, NW, DR, NM, kRegress>(a, n_blocks, s);
+    case kDerive: return launch_k<K, TM, R, NW, DR, NM, kDerive>(a, n_blocks, s);
     default: return hipErrorInvalidValue;
   }
 }
 
 }  // namespace
 
-// Instantiations: k in {16, 32, 64}; float64 with one wavefront per SIMD,
-// float32 with two; 16 atoms per tile except float64 at k = 64, whose moment
-// tiles need 8 to fit in LDS.  The other fusion configurations are built for
-// k = 32 only.
-int fused_tile_max(int k, int precision) { return (k == 64 && precision == 64) ? 8 : 16; }
+// Angular configurations: 0 = irreducible basis with l_max <= 3 (16 rows,
+// 20 monomials), 1 = Cartesian basis with l_max <= 3 (20 rows in two 16-row
+// tiles), 2 = irreducible basis with l_max 4 or 5 (up to 36 rows in three
+// tiles, 56 monomials of degree <= 5).
+int angular_config(int angular, int lmax) { return angular == 1 ? 1 : (lmax > 3 ? 2 : 0); }
 
-hipError_t launch_fused(int k, int precision, int mode, const FusedArgs& a, int n_blocks, hipStream_t s) {
-  if (mode != kCached && k != 32) return hipErrorInvalidValue;
+void angular_table_shape(int acfg, int* rows, int* cols) {
+  *rows = acfg == 0 ? 16 : (acfg == 1 ? 32 : 48);
+  *cols = acfg == 2 ? 56 : kMonomials;
+}
+
+// Instantiations: k in {16, 32, 64}; float64 with one wavefront per SIMD,
+// float32 with two; 16 atoms per tile except where the moment tiles would
+// not fit LDS (float64 at k = 64: 8; the wider angular configurations: 8 and
+// 4 in float64, 16 and 8 in float32).  The other fusion configurations and
+// the wider angular configurations are built for k = 32.
+int fused_tile_max(int k, int precision, int acfg) {
+  if (acfg == 1) return precision == 64 ? 8 : 16;
+  if (acfg == 2) return precision == 64 ? 4 : 8;
+  return (k == 64 && precision == 64) ? 8 : 16;
+}
+
+hipError_t launch_fused(int k, int precision, int acfg, int mode, const FusedArgs& a, int n_blocks, hipStream_t s) {
+  if ((mode != kCached || acfg != 0) && k != 32) return hipErrorInvalidValue;
+  if (acfg != 0 && mode != kCached) return hipErrorInvalidValue;
   if (precision == 64) {
+    if (acfg == 1) return launch_k<32, 8, double, 4, 32, 20, kCached>(a, n_blocks, s);
+    if (acfg == 2) return launch_k<32, 4, double, 4, 48, 56, kCached>(a, n_blocks, s);
     switch (k) {
-      case 16: return launch_k<16, 16, double, 4, kCached>(a, n_blocks, s);
-      case 32: return launch_mode<32, 16, double, 4>(mode, a, n_blocks, s);
-      case 64: return launch_k<64, 8, double, 4, kCached>(a, n_blocks, s);
+      case 16: return launch_k<16, 16, double, 4, 16, 20, kCached>(a, n_blocks, s);
+      case 32: return launch_mode<32, 16, double, 4, 16, 20>(mode, a, n_blocks, s);
+      case 64: return launch_k<64, 8, double, 4, 16, 20, kCached>(a, n_blocks, s);
       default: break;
     }
   } else if (precision == 32) {
+    if (acfg == 1) return launch_k<32, 16, float, 8, 32, 20, kCached>(a, n_blocks, s);
+    if (acfg == 2) return launch_k<32, 8, float, 8, 48, 56, kCached>(a, n_blocks, s);
     switch (k) {
-      case 16: return launch_k<16, 16, float, 8, kCached>(a, n_blocks, s);
-      case 32: return launch_mode<32, 16, float, 8>(mode, a, n_blocks, s);
-      case 64: return launch_k<64, 16, float, 8, kCached>(a, n_blocks, s);
+      case 16: return launch_k<16, 16, float, 8, 16, 20, kCached>(a, n_blocks, s);
+      case 32: return launch_mode<32, 16, float, 8, 16, 20>(mode, a, n_blocks, s);
+      case 64: return launch_k<64, 16, float, 8, 16, 20, kCached>(a, n_blocks, s);
       default: break;
     }
   }

@@ -7,6 +7,7 @@
 #include <cstddef>
 #include <cstdint>
 #include <string>
+#include <vector>
 
 #include "../../include/mlip.h"
 
@@ -58,6 +59,7 @@ struct FusedArgs {
   double box[3];
   double inv_box[3];
   double rc, rc2;
+  int lrow[8];                // first angular row of each order l, lrow[lmax+1] = d
   long long enc_stride, head_stride;
   int C, enc_cond, reg_cond, lmax, enc_hidden, reg_hidden;
   int tile_atoms;             // atoms per tile (<= fused_tile_max)
@@ -135,15 +137,20 @@ struct mlip_ctx {
   int64_t n_tiles = 0;
   int n_blocks = 0;
   int fusion = 0;                   // mlip_fusion
+  int acfg = 0;                     // angular configuration of the kernel
+  int lrow[8] = {0};                // first angular row of each order
   unsigned char* d_gbuf = nullptr;  // G / dE/dG per atom (three-kernel configuration), cap_gbuf bytes
   size_t cap_gbuf = 0;
 };
 
 namespace mlip {
 
-// angular_tables.cpp: coefficients of the irreducible angular features as
-// rows over the 20 Cartesian monomials of degree <= 3.
-bool build_angular_table(int lmax, double out[kAngRows * kMonomials], std::string* err);
+// angular_tables.cpp: coefficients of the angular features (angular 0
+// irreducible, 1 Cartesian) as rows over the Cartesian monomials, padded to
+// rows x cols, followed by one descriptor weight per row; lrow[l] = first row
+// of order l (lrow[lmax+1] = d).
+bool build_angular_table(int lmax, int angular, int rows, int cols, std::vector<double>* out, int lrow[8],
+                         std::string* err);
 
 // neighbors.hip
 hipError_t launch_bin(const double* pos, const int32_t* types, int64_t n, const NbrGrid& g,
@@ -165,11 +172,16 @@ hipError_t launch_fill_i32(int32_t* p, int64_t n, int32_t v, hipStream_t s);
 hipError_t launch_fill_f64(double* p, int64_t n, double v, hipStream_t s);
 hipError_t launch_fill_u64(unsigned long long* p, int64_t n, hipStream_t s);
 
-// fused.hip (k 16, 32 or 64; precision 64 or 32; mode: 0 cached, 1 recompute,
-// 2 encoding, 3 regression, 4 derivation kernel of the three-kernel split;
-// modes other than 0 for k = 32 only)
-hipError_t launch_fused(int k, int precision, int mode, const FusedArgs& a, int n_blocks, hipStream_t s);
-int fused_tile_max(int k, int precision);  // centre atoms per tile of that instantiation
+// fused.hip.  k 16, 32 or 64; precision 64 or 32; angular configuration
+// acfg 0 (irreducible, l_max <= 3: 16 rows x 20 monomials), 1 (Cartesian,
+// l_max <= 3: 32 x 20) or 2 (irreducible, l_max 4..5: 48 x 56); mode 0
+// cached, 1 recompute, 2 encoding, 3 regression, 4 derivation kernel of the
+// three-kernel split.  Configurations other than acfg 0 / mode 0 exist for
+// k = 32, and acfg 1, 2 only with mode 0.
+int angular_config(int angular, int lmax);
+void angular_table_shape(int acfg, int* rows, int* cols);
+int fused_tile_max(int k, int precision, int acfg);  // centre atoms per tile of that instantiation
+hipError_t launch_fused(int k, int precision, int acfg, int mode, const FusedArgs& a, int n_blocks, hipStream_t s);
 
 // md.hip
 hipError_t launch_md_first_half(double* pos, double* vel, const double* forces, const int32_t* types,

@@ -61,6 +61,8 @@ VARIANTS = {
     "deep": {"enc_hidden": 5, "reg_hidden": 6},
     "k16": {"k": 16},
     "k64": {"k": 64},
+    "cartesian": {"angular": 1},
+    "lmax5": {"lmax": 5},
 }
 
 

@@ -58,6 +58,10 @@ VARIANTS = {
     "k64": {"k": 64},
     "k64_lmax1_universal": {"k": 64, "lmax": 1, "enc_cond": 0},
     "k16_lmax0": {"k": 16, "lmax": 0},
+    "cartesian": {"angular": 1},
+    "cartesian_lmax2_universal": {"angular": 1, "lmax": 2, "enc_cond": 0},
+    "lmax4": {"lmax": 4},
+    "lmax5": {"lmax": 5},
 }
 
 
@@ -72,6 +76,14 @@ def test_binary_fcc_variants(variant):
 def test_preset_shapes(name, n):
     w = synth.make_workload(name, seed=5, n=n)
     _compare(w.hp, w.weights, w.pos, w.types, w.box, f"{name}/n={n}")
+
+
+@pytest.mark.parametrize("over", [{"angular": 1}, {"lmax": 5}])
+def test_angular_sweep_six_species(over):
+    """The Cartesian d = 20 basis and l_max = 5 (d = 36) on the 6-component
+    FCC shape (several angular row tiles, multi-tile moments)."""
+    w = synth.make_workload("fcc-hea6-128", seed=8, n=5, hp_overrides=over)
+    _compare(w.hp, w.weights, w.pos, w.types, w.box, f"fcc-hea6-128/n=5/{over}")
 
 
 @pytest.mark.parametrize("k", [16, 64])

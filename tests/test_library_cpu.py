@@ -55,7 +55,8 @@ def test_invalid_hparams(binding):
         assert binding.mlip_weight_count(hp) == 0
 
 
-@pytest.mark.parametrize("over", [{"k": 24}, {"lmax": 4}, {"angular": 1}, {"enc_width": 64},
+@pytest.mark.parametrize("over", [{"k": 24}, {"lmax": 6}, {"angular": 1, "lmax": 4}, {"angular": 1, "k": 16},
+                                  {"lmax": 5, "k": 64}, {"enc_width": 64},
                                   {"reg_width": 32}, {"precision": 16}, {"n_species": 17}, {"enc_hidden": 9}])
 def test_create_rejects_unsupported_before_device(binding, over):
     hp = synth.HParams(n_species=2)
