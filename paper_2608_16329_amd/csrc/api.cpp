@@ -400,6 +400,7 @@ mlip_status mlip_compute(mlip_ctx* ctx, const double* pos_dev, double* energy_de
   }
   a.rc = ctx->hp.cutoff;
   a.rc2 = ctx->hp.cutoff * ctx->hp.cutoff;
+  a.pi_rc = M_PI / ctx->hp.cutoff;
   a.enc_stride = (long long)ctx->enc_stride;
   a.head_stride = (long long)ctx->head_stride;
   a.C = ctx->hp.n_species;

@@ -500,7 +500,7 @@ __device__ void pass1_chunk(const FusedArgs& A, Smem<K, TM, R, NW, DR, NM>& S, i
   double uxd, uyd, uzd;
   int atom;
   const double rd = pair_distance(A, S, ch, pp, &uxd, &uyd, &uzd, &atom);
-  const double fcd = atom >= 0 ? 0.5 * (1.0 + cos(M_PI * rd / A.rc)) : 0.0;
+  const double fcd = atom >= 0 ? 0.5 * (1.0 + cos(rd * A.pi_rc)) : 0.0;
   const R r = R(rd), ux = R(uxd), uy = R(uyd), uz = R(uzd), fc = R(fcd);
 
   R h[8][4], dh[8][4];
@@ -634,9 +634,9 @@ __device__ void pass2_chunk(const FusedArgs& A, Smem<K, TM, R, NW, DR, NM>& S, i
   }
   const double ir = 1.0 / r;
   const double ux = dx * ir, uy = dy * ir, uz = dz * ir;
-  const double arg = M_PI * r / A.rc;
+  const double arg = r * A.pi_rc;
   const R fc = valid ? R(0.5 * (1.0 + cos(arg))) : R(0);
-  const R dfc = valid ? R(-0.5 * M_PI / A.rc * sin(arg)) : R(0);
+  const R dfc = valid ? R(-0.5 * A.pi_rc * sin(arg)) : R(0);
 
   // (W m) and (W dm) for this column's own centre atom, one 16-row tile of
   // the angular features at a time
@@ -665,30 +665,38 @@ __device__ void pass2_chunk(const FusedArgs& A, Smem<K, TM, R, NW, DR, NM>& S, i
   }
 
   // angular features a_mm and gradients for rows mm = 16 ta + drow(q, g) of
-  // this pair
+  // this pair, accumulated monomial by monomial so that each monomial and
+  // its gradient are live only for their own step
   R mono[NM], gx[NM], gy[NM], gz[NM];
   monomials_n<NM, true>(R(ux), R(uy), R(uz), mono, gx, gy, gz);
+  R fv[NA][4], fgx[NA][4], fgy[NA][4], fgz[NA][4];
+#pragma unroll
+  for (int ta = 0; ta < NA; ++ta)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) fv[ta][q] = fgx[ta][q] = fgy[ta][q] = fgz[ta][q] = R(0);
+#pragma unroll
+  for (int m = 0; m < NM; ++m)
+#pragma unroll
+    for (int ta = 0; ta < NA; ++ta)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const R co = S.qc[16 * ta + drow<R>(q, g)][m];
+        fv[ta][q] += co * mono[m];
+        fgx[ta][q] += co * gx[m];
+        fgy[ta][q] += co * gy[m];
+        fgz[ta][q] += co * gz[m];
+      }
   R s = 0, tx = 0, ty = 0, tz = 0;
 #pragma unroll
   for (int ta = 0; ta < NA; ++ta)
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
-      const int mm = 16 * ta + drow<R>(q, g);
-      R a_v = 0, a_x = 0, a_y = 0, a_z = 0;
-#pragma unroll
-      for (int m = 0; m < NM; ++m) {
-        const R co = S.qc[mm][m];
-        a_v += co * mono[m];
-        a_x += co * gx[m];
-        a_y += co * gy[m];
-        a_z += co * gz[m];
-      }
       const R v = fc * wm[ta][q];                       // v = W g
       const R wg = dfc * wm[ta][q] + fc * wdm[ta][q];   // W g'
-      s += a_v * wg;
-      tx += a_x * v;
-      ty += a_y * v;
-      tz += a_z * v;
+      s += fv[ta][q] * wg;
+      tx += fgx[ta][q] * v;
+      ty += fgy[ta][q] * v;
+      tz += fgz[ta][q] * v;
     }
 #pragma unroll
   for (int o = 16; o <= 32; o <<= 1) {
@@ -794,8 +802,19 @@ __device__ void head_stage(const FusedArgs& A, Smem<K, TM, R, NW, DR, NM>& S) {
   v4<R> z0 = v4<R>{0, 0, 0, 0};
   if (rw) {
     z0 = v4<R>{c0[ROW(0)], c0[ROW(1)], c0[ROW(2)], c0[ROW(3)]};
-    for (int ks = 0; ks < nin / 4; ++ks)
-      z0 = mfma(A0f[(ks * 4 + w) * 64 + lane], S.u.hd.xT[16 * (ks >> 2) + drow<R>(ks & 3, g)][c], z0);
+    // nin / 4 k-steps, a multiple of 4: fragments of 4 k-steps are loaded
+    // together and two accumulators alternate
+    v4<R> z0b = v4<R>{0, 0, 0, 0};
+    for (int k4 = 0; k4 < nin / 16; ++k4) {
+      R fa[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) fa[i] = A0f[((4 * k4 + i) * 4 + w) * 64 + lane];
+      z0 = mfma(fa[0], S.u.hd.xT[16 * k4 + drow<R>(0, g)][c], z0);
+      z0b = mfma(fa[1], S.u.hd.xT[16 * k4 + drow<R>(1, g)][c], z0b);
+      z0 = mfma(fa[2], S.u.hd.xT[16 * k4 + drow<R>(2, g)][c], z0);
+      z0b = mfma(fa[3], S.u.hd.xT[16 * k4 + drow<R>(3, g)][c], z0b);
+    }
+    z0 += z0b;
 #pragma unroll
     for (int q = 0; q < 4; ++q) S.u.hd.yT[ROW(q)][c] = z0[q] * sigmoid(z0[q]);
   }
@@ -1091,6 +1110,8 @@ __global__ __launch_bounds__(64 * NW, 1) void k_fused(FusedArgs A) {
 
     // ---- D: pass 2 ---------------------------------------------------------
     if constexpr (MODE == kCached || MODE == kDerive) {
+      // the workspace was written a whole pass earlier and comes back from
+      // beyond L2: inputs are loaded two chunks ahead
       Pass2In<K, R> next;
       if (wave < nch) pass2_load(A, S, wave, ws_slot + wave * chunk_elems, next);
       for (int ch = wave; ch < nch; ch += NW) {

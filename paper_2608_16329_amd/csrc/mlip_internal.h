@@ -59,6 +59,7 @@ struct FusedArgs {
   double box[3];
   double inv_box[3];
   double rc, rc2;
+  double pi_rc;               // pi / rc (cutoff function argument scale)
   int lrow[8];                // first angular row of each order l, lrow[lmax+1] = d
   long long enc_stride, head_stride;
   int C, enc_cond, reg_cond, lmax, enc_hidden, reg_hidden;
