@@ -350,13 +350,14 @@ mlip_status mlip_build_neighbors(mlip_ctx* ctx, int64_t n_atoms, const double* p
   ctx->max_row = flags[1];
 
   // fused-kernel tiling and workspace
-  const int T = std::max(1, std::min(fused_tile_max(ctx->hp.k, ctx->hp.precision, ctx->acfg), kEntCap / std::max(1, ctx->max_row)));
+  const int tm = fused_tile_max(ctx->hp.k, ctx->hp.precision, ctx->acfg);
+  const int T = std::max(1, std::min(tm, tile_entry_cap(tm) / std::max(1, ctx->max_row)));
   ctx->tile_atoms = T;
   int64_t tiles = 0;
   for (int sp_i = 0; sp_i < C; ++sp_i) tiles += (int64_t(sp[sp_i + 1] - sp[sp_i]) + T - 1) / T;
   ctx->n_tiles = tiles;
   ctx->n_blocks = int(std::max<int64_t>(1, std::min<int64_t>(tiles, ctx->n_cu)));
-  const int64_t chunks = std::min<int64_t>(kChunkCap, (int64_t(T) * ctx->max_row + 15) / 16 + C);
+  const int64_t chunks = std::min<int64_t>(tile_chunk_cap(tm), (int64_t(T) * ctx->max_row + 15) / 16 + C);
   ctx->ws_slot = size_t(chunks) * 2 * size_t(ctx->hp.k) * 16;
   MLIP_TRY(ensure(ctx, &ctx->d_ws, &ctx->cap_ws, ctx->ws_slot * size_t(ctx->n_blocks) * ctx->elem_bytes,
                   "workspace"));

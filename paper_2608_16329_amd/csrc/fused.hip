@@ -229,9 +229,9 @@ struct Smem {
   union {
     R l0[kMaxSpecies][2][kEncWidth];  // w0, b0 of the tile's encoder tables, by neighbour species
     struct {
-      R xT[(NM == 20 ? 4 : 6) * K][16];  // head input vec(G), feature-major
-      R yT[kHeadWidth][16];         // head activations
-      R gT[kHeadWidth][16];         // head backward scratch
+      R xT[(NM == 20 ? 4 : 6) * K][TM > 16 ? 32 : 16];  // head input vec(G), feature-major
+      R yT[kHeadWidth][TM > 16 ? 32 : 16];             // head activations
+      R gT[kHeadWidth][TM > 16 ? 32 : 16];             // head backward scratch
     } hd;
   } u;
   R qc[DR][NM];        // angular features over the monomials
@@ -245,14 +245,15 @@ struct Smem {
   int orig[TM];
   int cnt[kMaxSpecies][TM];
   int base[kMaxSpecies][TM];
-  int pair_j[kEntCap];
-  unsigned char pair_a[kEntCap];
+  int pair_j[tile_entry_cap(TM)];
+  unsigned char pair_a[tile_entry_cap(TM)];
   int wsum[NW];
   int a0;
-  int ch_start[kChunkCap];
-  unsigned char ch_count[kChunkCap];
-  unsigned char ch_s[kChunkCap];
+  int ch_start[tile_chunk_cap(TM)];
+  unsigned char ch_count[tile_chunk_cap(TM)];
+  unsigned char ch_s[tile_chunk_cap(TM)];
   int n_chunks;
+  int next_chunk[2];  // dynamic chunk hand-out of pass 1 and pass 2
   int n_active;
   int tile_species;
   int na;
@@ -263,6 +264,15 @@ struct Smem {
 struct PairPos {
   double x, y, z;
 };
+
+// Next chunk for this wavefront: chunks are handed out in order from an LDS
+// counter, so a wavefront that runs ahead of its SIMD partner takes more of
+// them and the wavefronts of a tile finish together.
+__device__ __forceinline__ int grab_chunk(int* counter) {
+  int v = 0;
+  if ((threadIdx.x & 63) == 0) v = atomicAdd(counter, 1);
+  return __builtin_amdgcn_readfirstlane(__shfl(v, 0, 64));
+}
 
 template <int K, int TM, typename R, int NW, int DR, int NM>
 __device__ __forceinline__ PairPos load_pair_pos(const FusedArgs& A, const Smem<K, TM, R, NW, DR, NM>& S, int ch) {
@@ -774,13 +784,15 @@ template <int K, int TM, typename R, int NW, int DR, int NM, bool kRegress>
 __device__ void head_stage(const FusedArgs& A, Smem<K, TM, R, NW, DR, NM>& S) {
   constexpr int RW = kHeadWidth;
   constexpr int HS = 2 * RW * RW + RW;  // one hidden layer: A_t and A_t^T fragments, c_t
+  constexpr int NC = TM > 16 ? 32 : 16;  // atom columns: one or two groups of 16
+  constexpr int CG = NC / 16;
   const int tid = threadIdx.x, lane = tid & 63, g = lane >> 4, c = lane & 15, w = tid >> 6;
   const int na = S.na;
   const int nin = (A.lmax + 1) * K;
   const int tin = nin / 16;
   R* __restrict__ gbuf = kRegress ? static_cast<R*>(A.gbuf) + (long long)S.a0 * nin : nullptr;
-  for (int u = tid; u < 16 * nin; u += (64 * NW)) {
-    const int a = u & 15, in = u >> 4;
+  for (int u = tid; u < NC * nin; u += (64 * NW)) {
+    const int a = u % NC, in = u / NC;
     R v = 0;
     if (a < na) v = kRegress ? gbuf[(long long)a * nin + in] : descriptor_value(A, S, a, in);
     S.u.hd.xT[in][a] = v;
@@ -794,51 +806,74 @@ __device__ void head_stage(const FusedArgs& A, Smem<K, TM, R, NW, DR, NM>& S) {
   const R* __restrict__ hid = c0 + RW;
   const R* __restrict__ aout = hid + (A.reg_hidden - 1) * HS;
   // this lane's result rows are 16 w + drow(q, g); with more than 4
-  // wavefronts the others only join the barriers of the row-parallel steps
+  // wavefronts the others only join the barriers of the row-parallel steps.
+  // Each weight fragment multiplies the CG column groups of atoms.
   const bool rw = w < RW / 16;
 #define ROW(q) (16 * w + drow<R>(q, g))
 
   // layer 0: z0 = A0 x + c0
-  v4<R> z0 = v4<R>{0, 0, 0, 0};
+  v4<R> z0[CG];
+#pragma unroll
+  for (int cg = 0; cg < CG; ++cg) z0[cg] = v4<R>{0, 0, 0, 0};
   if (rw) {
-    z0 = v4<R>{c0[ROW(0)], c0[ROW(1)], c0[ROW(2)], c0[ROW(3)]};
     // nin / 4 k-steps, a multiple of 4: fragments of 4 k-steps are loaded
     // together and two accumulators alternate
-    v4<R> z0b = v4<R>{0, 0, 0, 0};
+    v4<R> z0b[CG];
+#pragma unroll
+    for (int cg = 0; cg < CG; ++cg) {
+      z0[cg] = v4<R>{c0[ROW(0)], c0[ROW(1)], c0[ROW(2)], c0[ROW(3)]};
+      z0b[cg] = v4<R>{0, 0, 0, 0};
+    }
     for (int k4 = 0; k4 < nin / 16; ++k4) {
       R fa[4];
 #pragma unroll
       for (int i = 0; i < 4; ++i) fa[i] = A0f[((4 * k4 + i) * 4 + w) * 64 + lane];
-      z0 = mfma(fa[0], S.u.hd.xT[16 * k4 + drow<R>(0, g)][c], z0);
-      z0b = mfma(fa[1], S.u.hd.xT[16 * k4 + drow<R>(1, g)][c], z0b);
-      z0 = mfma(fa[2], S.u.hd.xT[16 * k4 + drow<R>(2, g)][c], z0);
-      z0b = mfma(fa[3], S.u.hd.xT[16 * k4 + drow<R>(3, g)][c], z0b);
-    }
-    z0 += z0b;
 #pragma unroll
-    for (int q = 0; q < 4; ++q) S.u.hd.yT[ROW(q)][c] = z0[q] * sigmoid(z0[q]);
+      for (int cg = 0; cg < CG; ++cg) {
+        z0[cg] = mfma(fa[0], S.u.hd.xT[16 * k4 + drow<R>(0, g)][16 * cg + c], z0[cg]);
+        z0b[cg] = mfma(fa[1], S.u.hd.xT[16 * k4 + drow<R>(1, g)][16 * cg + c], z0b[cg]);
+        z0[cg] = mfma(fa[2], S.u.hd.xT[16 * k4 + drow<R>(2, g)][16 * cg + c], z0[cg]);
+        z0b[cg] = mfma(fa[3], S.u.hd.xT[16 * k4 + drow<R>(3, g)][16 * cg + c], z0b[cg]);
+      }
+    }
+#pragma unroll
+    for (int cg = 0; cg < CG; ++cg) {
+      z0[cg] += z0b[cg];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) S.u.hd.yT[ROW(q)][16 * cg + c] = z0[cg][q] * sigmoid(z0[cg][q]);
+    }
   }
   __syncthreads();
 
   // residual layers: y <- y + silu(A_t y + c_t)
-  v4<R> zeta[kMaxHidden];
+  v4<R> zeta[kMaxHidden][CG];
 #pragma unroll
   for (int t = 1; t < kMaxHidden; ++t) {
     if (t >= A.reg_hidden) break;
     const R* __restrict__ Af = hid + (t - 1) * HS;
     const R* __restrict__ ct = Af + 2 * RW * RW;
-    v4<R> z = v4<R>{0, 0, 0, 0};
-    if (rw) {
-      z = v4<R>{ct[ROW(0)], ct[ROW(1)], ct[ROW(2)], ct[ROW(3)]};
+    v4<R> z[CG];
 #pragma unroll
-      for (int ks = 0; ks < 16; ++ks)
-        z = mfma(Af[(ks * 4 + w) * 64 + lane], S.u.hd.yT[16 * (ks >> 2) + drow<R>(ks & 3, g)][c], z);
+    for (int cg = 0; cg < CG; ++cg) z[cg] = v4<R>{0, 0, 0, 0};
+    if (rw) {
+#pragma unroll
+      for (int cg = 0; cg < CG; ++cg) z[cg] = v4<R>{ct[ROW(0)], ct[ROW(1)], ct[ROW(2)], ct[ROW(3)]};
+#pragma unroll
+      for (int ks = 0; ks < 16; ++ks) {
+        const R f = Af[(ks * 4 + w) * 64 + lane];
+#pragma unroll
+        for (int cg = 0; cg < CG; ++cg)
+          z[cg] = mfma(f, S.u.hd.yT[16 * (ks >> 2) + drow<R>(ks & 3, g)][16 * cg + c], z[cg]);
+      }
     }
-    zeta[t] = z;
+#pragma unroll
+    for (int cg = 0; cg < CG; ++cg) zeta[t][cg] = z[cg];
     __syncthreads();
     if (rw) {
 #pragma unroll
-      for (int q = 0; q < 4; ++q) S.u.hd.yT[ROW(q)][c] += z[q] * sigmoid(z[q]);
+      for (int cg = 0; cg < CG; ++cg)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) S.u.hd.yT[ROW(q)][16 * cg + c] += z[cg][q] * sigmoid(z[cg][q]);
     }
     __syncthreads();
   }
@@ -849,50 +884,74 @@ __device__ void head_stage(const FusedArgs& A, Smem<K, TM, R, NW, DR, NM>& S) {
   }
 
   // backward: d <- d + A_t^T (silu'(zeta_t) d), starting from d = a_out
-  v4<R> d = rw ? v4<R>{aout[ROW(0)], aout[ROW(1)], aout[ROW(2)], aout[ROW(3)]} : v4<R>{0, 0, 0, 0};
+  v4<R> d[CG];
+#pragma unroll
+  for (int cg = 0; cg < CG; ++cg)
+    d[cg] = rw ? v4<R>{aout[ROW(0)], aout[ROW(1)], aout[ROW(2)], aout[ROW(3)]} : v4<R>{0, 0, 0, 0};
 #pragma unroll
   for (int t = kMaxHidden - 1; t >= 1; --t) {
     if (t >= A.reg_hidden) continue;
     const R* __restrict__ ATf = hid + (t - 1) * HS + RW * RW;
     if (rw) {
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const R z = zeta[t][q], sg = sigmoid(z);
-        S.u.hd.gT[ROW(q)][c] = sg * (R(1) + z * (R(1) - sg)) * d[q];
-      }
+      for (int cg = 0; cg < CG; ++cg)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const R z = zeta[t][cg][q], sg = sigmoid(z);
+          S.u.hd.gT[ROW(q)][16 * cg + c] = sg * (R(1) + z * (R(1) - sg)) * d[cg][q];
+        }
     }
     __syncthreads();
     if (rw) {
-      v4<R> acc = v4<R>{0, 0, 0, 0};
+      v4<R> acc[CG];
 #pragma unroll
-      for (int ks = 0; ks < 16; ++ks)
-        acc = mfma(ATf[(ks * 4 + w) * 64 + lane], S.u.hd.gT[16 * (ks >> 2) + drow<R>(ks & 3, g)][c], acc);
-      d += acc;
+      for (int cg = 0; cg < CG; ++cg) acc[cg] = v4<R>{0, 0, 0, 0};
+#pragma unroll
+      for (int ks = 0; ks < 16; ++ks) {
+        const R f = ATf[(ks * 4 + w) * 64 + lane];
+#pragma unroll
+        for (int cg = 0; cg < CG; ++cg)
+          acc[cg] = mfma(f, S.u.hd.gT[16 * (ks >> 2) + drow<R>(ks & 3, g)][16 * cg + c], acc[cg]);
+      }
+#pragma unroll
+      for (int cg = 0; cg < CG; ++cg) d[cg] += acc[cg];
     }
     __syncthreads();
   }
   if (rw) {
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const R z = z0[q], sg = sigmoid(z);
-      S.u.hd.gT[ROW(q)][c] = sg * (R(1) + z * (R(1) - sg)) * d[q];
-    }
+    for (int cg = 0; cg < CG; ++cg)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const R z = z0[cg][q], sg = sigmoid(z);
+        S.u.hd.gT[ROW(q)][16 * cg + c] = sg * (R(1) + z * (R(1) - sg)) * d[cg][q];
+      }
   }
   __syncthreads();
   // dE/dx = A0^T g0, then W[0][col] = dE/dG[0][col], W[m][col] = 2 dE/dG[l][col] P[m][col]
   for (int tt = w; tt < tin; tt += NW) {
-    v4<R> acc = v4<R>{0, 0, 0, 0};
+    v4<R> acc[CG];
 #pragma unroll
-    for (int ks = 0; ks < 16; ++ks)
-      acc = mfma(A0Tf[(ks * tin + tt) * 64 + lane], S.u.hd.gT[16 * (ks >> 2) + drow<R>(ks & 3, g)][c], acc);
-    if (c < na) {
+    for (int cg = 0; cg < CG; ++cg) acc[cg] = v4<R>{0, 0, 0, 0};
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const int in = 16 * tt + drow<R>(q, g);
-        if (kRegress)
-          gbuf[(long long)c * nin + in] = acc[q];
-        else
-          adjoint_from_grad(A, S, c, in, acc[q]);
+    for (int ks = 0; ks < 16; ++ks) {
+      const R f = A0Tf[(ks * tin + tt) * 64 + lane];
+#pragma unroll
+      for (int cg = 0; cg < CG; ++cg)
+        acc[cg] = mfma(f, S.u.hd.gT[16 * (ks >> 2) + drow<R>(ks & 3, g)][16 * cg + c], acc[cg]);
+    }
+#pragma unroll
+    for (int cg = 0; cg < CG; ++cg) {
+      const int a = 16 * cg + c;
+      if (a < na) {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int in = 16 * tt + drow<R>(q, g);
+          if (kRegress)
+            gbuf[(long long)a * nin + in] = acc[cg][q];
+          else
+            adjoint_from_grad(A, S, a, in, acc[cg][q]);
+        }
       }
     }
   }
@@ -986,7 +1045,7 @@ __global__ __launch_bounds__(64 * NW, 1) void k_fused(FusedArgs A) {
     __syncthreads();
     const int nent = S.ent_base[na];
     const long long ebase = S.row_beg[0];
-    constexpr int kPer = kEntCap / (64 * NW);
+    constexpr int kPer = tile_entry_cap(TM) / (64 * NW);
     int ej[kPer], ea[kPer], es[kPer];
     int my_active = 0;
     {
@@ -1047,6 +1106,8 @@ __global__ __launch_bounds__(64 * NW, 1) void k_fused(FusedArgs A) {
         }
       }
       S.n_chunks = nch;
+      S.next_chunk[0] = NW;  // chunk w < NW starts on wavefront w
+      S.next_chunk[1] = NW;
       S.n_active = run;
       int row_start = 0;
       for (int a = 0; a < na; ++a) {
@@ -1079,11 +1140,14 @@ __global__ __launch_bounds__(64 * NW, 1) void k_fused(FusedArgs A) {
     nch = S.n_chunks;
     {
       constexpr bool kWs = MODE == kCached || MODE == kDerive;
-      PairPos next = wave < nch ? load_pair_pos(A, S, wave) : PairPos{0.0, 0.0, 0.0};
-      for (int ch = wave; ch < nch; ch += NW) {
+      int ch = wave;
+      PairPos next = ch < nch ? load_pair_pos(A, S, ch) : PairPos{0.0, 0.0, 0.0};
+      while (ch < nch) {
         const PairPos cur = next;
-        if (ch + NW < nch) next = load_pair_pos(A, S, ch + NW);
+        const int ch2 = grab_chunk(&S.next_chunk[0]);
+        if (ch2 < nch) next = load_pair_pos(A, S, ch2);
         pass1_chunk<K, TM, R, NW, DR, NM, kWs>(A, S, ch, cur, ws_slot + ch * chunk_elems);
+        ch = ch2;
       }
     }
     __syncthreads();
@@ -1110,26 +1174,31 @@ __global__ __launch_bounds__(64 * NW, 1) void k_fused(FusedArgs A) {
 
     // ---- D: pass 2 ---------------------------------------------------------
     if constexpr (MODE == kCached || MODE == kDerive) {
-      // the workspace was written a whole pass earlier and comes back from
-      // beyond L2: inputs are loaded two chunks ahead
+      // inputs of the next chunk are loaded while this one is processed
+      int ch = wave;
       Pass2In<K, R> next;
-      if (wave < nch) pass2_load(A, S, wave, ws_slot + wave * chunk_elems, next);
-      for (int ch = wave; ch < nch; ch += NW) {
+      if (ch < nch) pass2_load(A, S, ch, ws_slot + ch * chunk_elems, next);
+      while (ch < nch) {
         const Pass2In<K, R> cur = next;
-        if (ch + NW < nch) pass2_load(A, S, ch + NW, ws_slot + (ch + NW) * chunk_elems, next);
+        const int ch2 = grab_chunk(&S.next_chunk[1]);
+        if (ch2 < nch) pass2_load(A, S, ch2, ws_slot + ch2 * chunk_elems, next);
         pass2_chunk<K, TM, R, NW, DR, NM>(A, S, ch, cur);
+        ch = ch2;
       }
     } else if constexpr (MODE == kRecompute) {
       // the head's activations overwrote the first-layer weights in LDS
       stage_first_layer(A, S, enc);
       __syncthreads();
-      PairPos next = wave < nch ? load_pair_pos(A, S, wave) : PairPos{0.0, 0.0, 0.0};
-      for (int ch = wave; ch < nch; ch += NW) {
+      int ch = wave;
+      PairPos next = ch < nch ? load_pair_pos(A, S, ch) : PairPos{0.0, 0.0, 0.0};
+      while (ch < nch) {
         const PairPos cur = next;
-        if (ch + NW < nch) next = load_pair_pos(A, S, ch + NW);
+        const int ch2 = grab_chunk(&S.next_chunk[1]);
+        if (ch2 < nch) next = load_pair_pos(A, S, ch2);
         Pass2In<K, R> in;
         pass2_recompute(A, S, ch, cur, in);
         pass2_chunk<K, TM, R, NW, DR, NM>(A, S, ch, in);
+        ch = ch2;
       }
     }
     __syncthreads();
@@ -1214,14 +1283,16 @@ void angular_table_shape(int acfg, int* rows, int* cols) {
 }
 
 // Instantiations: k in {16, 32, 64}; float64 with one wavefront per SIMD,
-// float32 with two; 16 atoms per tile except where the moment tiles would
-// not fit LDS (float64 at k = 64: 8; the wider angular configurations: 8 and
-// 4 in float64, 16 and 8 in float32).  The other fusion configurations and
+// float32 with two.  Atoms per tile: float64 16, float32 32 (two column
+// groups in the head), fewer where the moment tiles would not fit LDS
+// (float64 at k = 64: 8; float32 at k = 64: 16; the wider angular
+// configurations: 8 and 4 in float64, 16 and 8 in float32).  The other fusion configurations and
 // the wider angular configurations are built for k = 32.
 int fused_tile_max(int k, int precision, int acfg) {
   if (acfg == 1) return precision == 64 ? 8 : 16;
   if (acfg == 2) return precision == 64 ? 4 : 8;
-  return (k == 64 && precision == 64) ? 8 : 16;
+  if (precision == 64) return k == 64 ? 8 : 16;
+  return k == 64 ? 16 : 32;
 }
 
 hipError_t launch_fused(int k, int precision, int acfg, int mode, const FusedArgs& a, int n_blocks, hipStream_t s) {
@@ -1240,8 +1311,8 @@ hipError_t launch_fused(int k, int precision, int acfg, int mode, const FusedArg
     if (acfg == 1) return launch_k<32, 16, float, 8, 32, 20, kCached>(a, n_blocks, s);
     if (acfg == 2) return launch_k<32, 8, float, 8, 48, 56, kCached>(a, n_blocks, s);
     switch (k) {
-      case 16: return launch_k<16, 16, float, 8, 16, 20, kCached>(a, n_blocks, s);
-      case 32: return launch_mode<32, 16, float, 8, 16, 20>(mode, a, n_blocks, s);
+      case 16: return launch_k<16, 32, float, 8, 16, 20, kCached>(a, n_blocks, s);
+      case 32: return launch_mode<32, 32, float, 8, 16, 20>(mode, a, n_blocks, s);
       case 64: return launch_k<64, 16, float, 8, 16, 20, kCached>(a, n_blocks, s);
       default: break;
     }

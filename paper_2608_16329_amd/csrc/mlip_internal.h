@@ -16,8 +16,10 @@ namespace mlip {
 // Fused-kernel geometry (gfx950: 64-wide wavefronts, 160 KB LDS per CU).
 constexpr int kWaves = 4;                 // wavefronts per work-group (one per SIMD)
 constexpr int kThreads = kWaves * 64;     // work-group size
-constexpr int kEntCap = 2048;             // listed neighbour entries per tile
-constexpr int kChunkCap = kEntCap / 16 + 16;
+constexpr int kEntCap = 2048;             // longest neighbour row
+// Listed entries and chunks one tile of tm atoms can hold.
+constexpr int tile_entry_cap(int tm) { return tm * 128 > kEntCap ? tm * 128 : kEntCap; }
+constexpr int tile_chunk_cap(int tm) { return tile_entry_cap(tm) / 16 + 16; }
 constexpr int kMaxSpecies = 16;
 constexpr int kEncWidth = 128;            // encoder hidden width on the GPU path
 constexpr int kHeadWidth = 64;            // head hidden width on the GPU path
