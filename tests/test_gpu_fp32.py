@@ -135,3 +135,44 @@ def test_fp32_full_size_sampled():
     log(f"[fp32] full size sampled: rel dE={eE:.2e} dF={eF:.2e} dW={eV:.2e}")
     assert eE <= REL_TOL and eF <= REL_TOL and eV <= REL_TOL
     pot.close()
+
+
+def test_fp32_long_rows_small_tiles():
+    """About 700 listed neighbours per atom: the 32-atom float32 tiles shrink
+    to 4096 / max_row atoms (weights scaled by 0.3 as in the float64 test)."""
+    rng = np.random.default_rng(31)
+    hp = synth.HParams(n_species=3, cutoff=12.0, skin=0.5)
+    pos, box = synth.lattice("fcc", 7, 3.6)
+    pos = pos + rng.normal(0.0, 0.1, pos.shape)
+    types = rng.integers(0, 3, len(pos)).astype(np.int32)
+    g, _ = _compare(hp, synth.random_weights(hp, 4, 0.3), pos, types, box, "long rows")
+    assert g["stats"]["max_row"] > 600 and g["stats"]["tile_atoms"] == 4096 // g["stats"]["max_row"]
+
+
+def test_fp32_md_trajectory():
+    """Ten velocity-Verlet steps with the float32 network; every step is fed
+    to the oracle at the GPU's own positions."""
+    import torch
+    from paper_2608_16329_amd import Potential
+    w = synth.make_workload("fcc-binary-4", seed=1, hp_overrides={"precision": 32})
+    m = Model(w.hp, w.weights)
+    pot = Potential(w.hp, w.weights)
+    pot.set_masses(w.masses)
+    pos, vel, types = to_dev(w.pos), to_dev(w.vel), to_dev(w.types)
+    ref = pos.clone()
+    F = torch.zeros((len(w.pos), 3), dtype=torch.float64, device="cuda:0")
+    pot.build_neighbors(pos, types, w.box)
+    pot.compute(pos, F)
+    for step in range(1, 11):
+        d2 = pot.md_first_half(pos, vel, F, 1.0, ref)
+        if step % 10 == 0 or d2 > (0.5 * w.hp.skin) ** 2:
+            pot.build_neighbors(pos, types, w.box)
+            ref.copy_(pos)
+        pot.compute(pos, F)
+        pot.md_second_half(vel, F, 1.0)
+        torch.cuda.synchronize()
+        r = evaluate(m, pos.cpu().numpy(), w.types, w.box)
+        e = rel_err(F.cpu().numpy(), r["F"])
+        log(f"[fp32] md step {step}: rel dF={e:.2e}")
+        assert e <= REL_TOL
+    pot.close()
