@@ -136,7 +136,9 @@ mlip_status mlip_create(const mlip_hparams* hp, const double* weights_host, size
  * vector dx = w_j - w_i folded once by -L if dx > L/2 or +L if dx < -L/2;
  * d2 = (dx*dx + dy*dy) + dz*dz without fused multiply-add; j != i is listed
  * iff d2 < (cutoff + skin)^2.  Rows are grouped by neighbour species.
- *   n_atoms   number of atoms (>= 1, < 2^31)
+ *   n_atoms   number of atoms (>= 0, < 2^31).  0 records an empty system
+ *             (the pointers may then be NULL): later calls succeed and
+ *             produce nothing, totals and kinetic energy 0
  *   pos_dev   float64 [n_atoms][3], any real values (wrapped internally)
  *   types_dev int32 [n_atoms], species in [0, n_species); copied
  *   box_host  float64 [3], orthorhombic periodic box edges L_x, L_y, L_z

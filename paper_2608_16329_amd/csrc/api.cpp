@@ -260,14 +260,28 @@ mlip_status mlip_build_neighbors(mlip_ctx* ctx, int64_t n_atoms, const double* p
                                  const double box_host[3]) {
   if (!ctx) return MLIP_E_ARG;
   ctx->err.clear();
-  if (!pos_dev || !types_dev || !box_host) return fail(ctx, MLIP_E_ARG, "NULL argument");
-  if (n_atoms < 1 || n_atoms >= (int64_t(1) << 31)) return fail(ctx, MLIP_E_ARG, "n_atoms outside [1, 2^31)");
+  if (!box_host) return fail(ctx, MLIP_E_ARG, "NULL box");
+  if (n_atoms < 0 || n_atoms >= (int64_t(1) << 31)) return fail(ctx, MLIP_E_ARG, "n_atoms outside [0, 2^31)");
+  if (n_atoms > 0 && (!pos_dev || !types_dev)) return fail(ctx, MLIP_E_ARG, "NULL argument");
   const double rl = ctx->hp.cutoff + ctx->hp.skin;
   for (int d = 0; d < 3; ++d)
     if (!(box_host[d] > 0.0) || !std::isfinite(box_host[d])) return fail(ctx, MLIP_E_BOX, "box edges must be positive");
   const double lmin = std::min(box_host[0], std::min(box_host[1], box_host[2]));
   if (!(rl <= 0.5 * lmin)) return fail(ctx, MLIP_E_BOX, "cutoff + skin exceeds half the smallest box edge");
   ctx->built = false;
+  if (n_atoms == 0) {
+    // an empty system: nothing to bin; later calls produce nothing
+    ctx->n = 0;
+    for (int d = 0; d < 3; ++d) ctx->box[d] = box_host[d];
+    for (int i = 0; i <= kMaxSpecies; ++i) ctx->species_start[i] = 0;
+    ctx->n_listed = 0;
+    ctx->max_row = 0;
+    ctx->tile_atoms = 0;
+    ctx->n_tiles = 0;
+    ctx->built = true;
+    ctx->n_builds += 1;
+    return MLIP_OK;
+  }
   const int64_t n = n_atoms;
   const int C = ctx->hp.n_species;
   hipStream_t s = ctx->stream;
@@ -370,10 +384,15 @@ mlip_status mlip_compute(mlip_ctx* ctx, const double* pos_dev, double* energy_de
                          double* virial_dev, double* totals_host) {
   if (!ctx) return MLIP_E_ARG;
   ctx->err.clear();
-  if (!pos_dev || !forces_dev) return fail(ctx, MLIP_E_ARG, "NULL positions or forces");
   if (!ctx->built) return fail(ctx, MLIP_E_STATE, "mlip_build_neighbors has not been called");
   hipStream_t s = ctx->stream;
   const int64_t n = ctx->n;
+  if (n == 0) {
+    if (totals_host)
+      for (int k = 0; k < 10; ++k) totals_host[k] = 0.0;
+    return MLIP_OK;
+  }
+  if (!pos_dev || !forces_dev) return fail(ctx, MLIP_E_ARG, "NULL positions or forces");
   MLIP_HIP(ctx, launch_fill_f64(forces_dev, 3 * n, 0.0, s));
   MLIP_HIP(ctx, launch_fill_f64(ctx->d_totals, 16, 0.0, s));
   MLIP_HIP(ctx, launch_fill_u64(ctx->d_counters, 4, s));
@@ -445,6 +464,10 @@ mlip_status mlip_get_neighbors(mlip_ctx* ctx, int64_t* offsets_host, int32_t* id
   if (!offsets_host || !idx_host) return fail(ctx, MLIP_E_ARG, "NULL argument");
   if (!ctx->built) return fail(ctx, MLIP_E_STATE, "no neighbour list");
   const int64_t n = ctx->n;
+  if (n == 0) {
+    offsets_host[0] = 0;
+    return MLIP_OK;
+  }
   std::vector<int64_t> off(size_t(n + 1));
   std::vector<int32_t> perm(static_cast<size_t>(n));
   std::vector<int32_t> idx(static_cast<size_t>(std::max<int64_t>(ctx->n_listed, 1)));
@@ -539,8 +562,12 @@ mlip_status mlip_md_set_masses(mlip_ctx* ctx, const double* masses_host) {
 mlip_status mlip_md_first_half(mlip_ctx* ctx, double* pos_dev, double* vel_dev, const double* forces_dev, double dt,
                                const double* ref_dev, double* max_disp2_host) {
   if (!ctx) return MLIP_E_ARG;
-  if (!pos_dev || !vel_dev || !forces_dev) return fail(ctx, MLIP_E_ARG, "NULL argument");
   if (!ctx->built || !ctx->masses_set) return fail(ctx, MLIP_E_STATE, "build neighbours and set masses first");
+  if (ctx->n == 0) {
+    if (max_disp2_host) *max_disp2_host = 0.0;
+    return MLIP_OK;
+  }
+  if (!pos_dev || !vel_dev || !forces_dev) return fail(ctx, MLIP_E_ARG, "NULL argument");
   const bool track = max_disp2_host != nullptr;
   if (track) MLIP_HIP(ctx, launch_fill_f64(ctx->d_reduce, 1, 0.0, ctx->stream));
   MLIP_HIP(ctx, launch_md_first_half(pos_dev, vel_dev, forces_dev, ctx->d_types, ctx->d_inv_mass, ctx->n, dt,
@@ -557,16 +584,22 @@ mlip_status mlip_md_first_half(mlip_ctx* ctx, double* pos_dev, double* vel_dev, 
 
 mlip_status mlip_md_second_half(mlip_ctx* ctx, double* vel_dev, const double* forces_dev, double dt) {
   if (!ctx) return MLIP_E_ARG;
-  if (!vel_dev || !forces_dev) return fail(ctx, MLIP_E_ARG, "NULL argument");
   if (!ctx->built || !ctx->masses_set) return fail(ctx, MLIP_E_STATE, "build neighbours and set masses first");
+  if (ctx->n == 0) return MLIP_OK;
+  if (!vel_dev || !forces_dev) return fail(ctx, MLIP_E_ARG, "NULL argument");
   MLIP_HIP(ctx, launch_md_second_half(vel_dev, forces_dev, ctx->d_types, ctx->d_inv_mass, ctx->n, dt, ctx->stream));
   return MLIP_OK;
 }
 
 mlip_status mlip_md_kinetic(mlip_ctx* ctx, const double* vel_dev, double* ke_host) {
   if (!ctx) return MLIP_E_ARG;
-  if (!vel_dev || !ke_host) return fail(ctx, MLIP_E_ARG, "NULL argument");
+  if (!ke_host) return fail(ctx, MLIP_E_ARG, "NULL argument");
   if (!ctx->built || !ctx->masses_set) return fail(ctx, MLIP_E_STATE, "build neighbours and set masses first");
+  if (ctx->n == 0) {
+    *ke_host = 0.0;
+    return MLIP_OK;
+  }
+  if (!vel_dev) return fail(ctx, MLIP_E_ARG, "NULL argument");
   MLIP_HIP(ctx, launch_fill_f64(ctx->d_reduce + 1, 1, 0.0, ctx->stream));
   MLIP_HIP(ctx, launch_md_kinetic(vel_dev, ctx->d_types, ctx->d_inv_mass, ctx->n, ctx->d_reduce + 1, ctx->stream));
   MLIP_HIP(ctx, hipMemcpyAsync(ke_host, ctx->d_reduce + 1, sizeof(double), hipMemcpyDeviceToHost, ctx->stream));

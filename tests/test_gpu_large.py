@@ -9,7 +9,7 @@ import pytest
 import synth
 from oracle.model import Model
 from oracle.neighbors import neighbors_of
-from tests.gpu_helpers import to_dev, oracle_sample, log
+from tests.gpu_helpers import to_dev, oracle_sample, log, max_abs
 
 pytestmark = pytest.mark.gpu
 
@@ -121,4 +121,31 @@ def test_bcc_unary_nve_100_steps_sampled():
             ref_rows = neighbors_of(p, w.box, w.hp.cutoff + w.hp.skin, atoms[:3])
             for a, r in zip(atoms[:3], ref_rows):
                 assert np.array_equal(np.sort(gidx[goff[a]:goff[a + 1]]), r)
+    pot.close()
+
+
+def test_bcc_six_component_sweep_shape_sampled():
+    """The capacity-sweep alloy (6-component BCC, a = 3.2 A) at L = 128
+    (4,194,304 atoms) in the launch configuration of the sweep: sampled
+    atoms against the oracle."""
+    import torch
+    from paper_2608_16329_amd import Potential
+    w = synth.make_workload("bcc-hea6-sweep", seed=0, n=128)
+    N = len(w.pos)
+    log(f"[large] bcc sweep shape N={N}")
+    pot = Potential(w.hp, w.weights)
+    p = to_dev(w.pos)
+    pot.build_neighbors(p, to_dev(w.types), w.box)
+    F = torch.empty((N, 3), dtype=torch.float64, device="cuda:0")
+    E = torch.empty(N, dtype=torch.float64, device="cuda:0")
+    V = torch.empty((N, 9), dtype=torch.float64, device="cuda:0")
+    pot.compute(p, F, E, V)
+    torch.cuda.synchronize()
+    atoms = np.random.default_rng(21).choice(N, 32, replace=False)
+    Er, Fr, Vr = oracle_sample(Model(w.hp, w.weights), w.pos, w.types, w.box, atoms)
+    eE = max_abs(E.cpu().numpy()[atoms], Er)
+    eF = max_abs(F.cpu().numpy()[atoms], Fr)
+    eV = max_abs(V.cpu().numpy()[atoms], Vr)
+    log(f"[large] bcc sweep shape: max|dE|={eE:.2e} max|dF|={eF:.2e} max|dW|={eV:.2e}")
+    assert max(eE, eF, eV) <= 1e-9
     pot.close()

@@ -213,6 +213,39 @@ def test_two_atoms_and_pair_at_cutoff():
     assert np.all(g["F"] == 0.0)
 
 
+def test_empty_system_then_real_one():
+    """n = 0 is an empty system: every call succeeds and produces nothing;
+    the same context then handles a real system."""
+    torch = pytest.importorskip("torch")
+    from paper_2608_16329_amd import Potential
+    w = synth.make_workload("fcc-binary-4", seed=4)
+    pot = Potential(w.hp, w.weights)
+    pot.set_masses(w.masses)
+    pos = torch.empty((0, 3), dtype=torch.float64, device="cuda:0")
+    types = torch.empty(0, dtype=torch.int32, device="cuda:0")
+    F = torch.empty((0, 3), dtype=torch.float64, device="cuda:0")
+    log("[edge] empty system")
+    pot.build_neighbors(pos, types, w.box)
+    tot = pot.compute(pos, F, totals=True)
+    assert np.all(tot == 0.0)
+    off, idx = pot.neighbors()
+    assert list(off) == [0] and len(idx) == 0
+    assert pot.stats()["n_atoms"] == 0
+    assert pot.md_first_half(pos, F, F, 1.0, track=True) == 0.0
+    pot.md_second_half(F, F, 1.0)
+    assert pot.kinetic(F) == 0.0
+    n = len(w.pos)
+    pos = to_dev(w.pos)
+    F = torch.zeros((n, 3), dtype=torch.float64, device="cuda:0")
+    E = torch.zeros(n, dtype=torch.float64, device="cuda:0")
+    pot.build_neighbors(pos, to_dev(w.types), w.box)
+    pot.compute(pos, F, E)
+    torch.cuda.synchronize()
+    ref = evaluate(Model(w.hp, w.weights), w.pos, w.types, w.box)
+    assert max_abs(F.cpu().numpy(), ref["F"]) <= TOL and max_abs(E.cpu().numpy(), ref["E_i"]) <= TOL
+    pot.close()
+
+
 def test_error_paths():
     from paper_2608_16329_amd import Potential, MlipError
     torch = pytest.importorskip("torch")
