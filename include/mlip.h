@@ -31,9 +31,9 @@
  *     the network is set by mlip_hparams.precision: 64 evaluates everything
  *     in float64 (Section 4.1); 32 is the reduced-precision mode the paper
  *     evaluates beside it (Sections 3.4 and 4.4), here with the network, the
- *     angular features and the moment/adjoint contractions in float32 and
- *     the pair geometry and all force, virial and energy accumulation in
- *     float64.
+ *     angular features, the moment/adjoint contractions and the pair
+ *     geometry after the minimum-image difference in float32, and that
+ *     difference and all force, virial and energy accumulation in float64.
  */
 #ifndef MLIP_H
 #define MLIP_H

@@ -28,10 +28,10 @@
 // The kernel is instantiated for two arithmetic types R of the network and
 // the contractions: float64 (the paper's evaluation precision, Section 4.1)
 // and float32 (the reduced-precision mode evaluated beside it, Sections 3.4
-// and 4.4).  Pair geometry (minimum image, r, unit vector, cutoff function)
-// and every output accumulation (F_i, F_j, w_i, E, totals) stay in float64
-// in both; the network, the angular features, the moment, W and the two
-// pass-2 contractions use R.
+// and 4.4).  The minimum-image difference of positions and every output
+// accumulation (F_i, F_j, w_i, E, totals) stay in float64 in both; r, the
+// unit vector, the cutoff function, the network, the angular features, the
+// moment, W, the two pass-2 contractions and the partial force use R.
 //
 // MFMA 16x16x4 register layout on gfx950 (lane = 16*g + c), for both types:
 //   A operand: lane holds A[c][g]; B operand: lane holds B[g][c].
@@ -135,6 +135,18 @@ __device__ __forceinline__ float sigmoid(float z) {
 }
 
 __device__ __forceinline__ double fold(double d, double L, double invL) { return d - L * rint(d * invL); }
+
+// Pair geometry after the minimum-image difference (which stays in float64):
+// IEEE float64 operations, or the float32 hardware instructions (about one
+// ulp; sine and cosine take revolutions, valid here since 0 <= x <= pi).
+__device__ __forceinline__ double vsqrt(double x) { return sqrt(x); }
+__device__ __forceinline__ float vsqrt(float x) { return __builtin_amdgcn_sqrtf(x); }
+__device__ __forceinline__ double vrcp(double x) { return 1.0 / x; }
+__device__ __forceinline__ float vrcp(float x) { return __builtin_amdgcn_rcpf(x); }
+__device__ __forceinline__ double vcos(double x) { return cos(x); }
+__device__ __forceinline__ float vcos(float x) { return __builtin_amdgcn_cosf(x * 0.159154943f); }
+__device__ __forceinline__ double vsin(double x) { return sin(x); }
+__device__ __forceinline__ float vsin(float x) { return __builtin_amdgcn_sinf(x * 0.159154943f); }
 
 // Cartesian monomials of degree <= 3 in the order of the angular table.
 template <typename R>
@@ -302,23 +314,19 @@ struct Stream {
   typedef R vo_t __attribute__((ext_vector_type(VO)));
 };
 
-// Distance of the pair in column c of chunk ch (Eq. 1), in float64; 1 for
-// the padding columns of a partial chunk.
+// Minimum-image vector r_ij of the pair in column c of chunk ch (Eq. 1), in
+// float64; (1, 0, 0) and atom -1 for the padding columns of a partial chunk.
 template <int K, int TM, typename R, int NW, int DR, int NM>
-__device__ __forceinline__ double pair_distance(const FusedArgs& A, const Smem<K, TM, R, NW, DR, NM>& S, int ch,
-                                                const PairPos& pp, double* ux, double* uy, double* uz, int* atom) {
+__device__ __forceinline__ void pair_delta(const FusedArgs& A, const Smem<K, TM, R, NW, DR, NM>& S, int ch,
+                                           const PairPos& pp, double* dx, double* dy, double* dz, int* atom) {
   const int c = threadIdx.x & 15;
-  *ux = 1.0; *uy = 0.0; *uz = 0.0; *atom = -1;
-  if (c >= S.ch_count[ch]) return 1.0;
+  *dx = 1.0; *dy = 0.0; *dz = 0.0; *atom = -1;
+  if (c >= S.ch_count[ch]) return;
   const int a = S.pair_a[S.ch_start[ch] + c];
-  const double dx = fold(pp.x - S.tpos[a][0], A.box[0], A.inv_box[0]);
-  const double dy = fold(pp.y - S.tpos[a][1], A.box[1], A.inv_box[1]);
-  const double dz = fold(pp.z - S.tpos[a][2], A.box[2], A.inv_box[2]);
-  const double r = sqrt(dx * dx + dy * dy + dz * dz);
-  const double ir = 1.0 / r;
-  *ux = dx * ir; *uy = dy * ir; *uz = dz * ir;
+  *dx = fold(pp.x - S.tpos[a][0], A.box[0], A.inv_box[0]);
+  *dy = fold(pp.y - S.tpos[a][1], A.box[1], A.inv_box[1]);
+  *dz = fold(pp.z - S.tpos[a][2], A.box[2], A.inv_box[2]);
   *atom = a;
-  return r;
 }
 
 // Encoder table of chunk ch (pair conditioning, Section 3.2).
@@ -507,11 +515,14 @@ __device__ void pass1_chunk(const FusedArgs& A, Smem<K, TM, R, NW, DR, NM>& S, i
   const int lane = threadIdx.x & 63, g = lane >> 4, c = lane & 15;
   const int start = S.ch_start[ch], count = S.ch_count[ch];
 
-  double uxd, uyd, uzd;
+  double dxd, dyd, dzd;
   int atom;
-  const double rd = pair_distance(A, S, ch, pp, &uxd, &uyd, &uzd, &atom);
-  const double fcd = atom >= 0 ? 0.5 * (1.0 + cos(rd * A.pi_rc)) : 0.0;
-  const R r = R(rd), ux = R(uxd), uy = R(uyd), uz = R(uzd), fc = R(fcd);
+  pair_delta(A, S, ch, pp, &dxd, &dyd, &dzd, &atom);
+  const R dx = R(dxd), dy = R(dyd), dz = R(dzd);
+  const R r = vsqrt(dx * dx + dy * dy + dz * dz);
+  const R ir = vrcp(r);
+  const R ux = dx * ir, uy = dy * ir, uz = dz * ir;
+  const R fc = atom >= 0 ? R(0.5) * (R(1) + vcos(r * R(A.pi_rc))) : R(0);
 
   R h[8][4], dh[8][4];
   const R* __restrict__ layer = encoder_hidden(A, S, S.ch_s[ch], r, chunk_table(A, S, ch), h, dh);
@@ -614,9 +625,11 @@ __device__ __forceinline__ void pass2_load(const FusedArgs& A, const Smem<K, TM,
 template <int K, int TM, typename R, int NW, int DR, int NM>
 __device__ __forceinline__ void pass2_recompute(const FusedArgs& A, const Smem<K, TM, R, NW, DR, NM>& S, int ch,
                                                 const PairPos& pp, Pass2In<K, R>& in) {
-  double ux, uy, uz;
+  double dxd, dyd, dzd;
   int atom;
-  const R r = R(pair_distance(A, S, ch, pp, &ux, &uy, &uz, &atom));
+  pair_delta(A, S, ch, pp, &dxd, &dyd, &dzd, &atom);
+  const R dx = R(dxd), dy = R(dyd), dz = R(dzd);
+  const R r = vsqrt(dx * dx + dy * dy + dz * dz);
   R h[8][4], dh[8][4];
   const R* __restrict__ layer = encoder_hidden(A, S, S.ch_s[ch], r, chunk_table(A, S, ch), h, dh);
   encoder_out_cols<K, R>(layer, h, dh, in.mB, in.dmB);
@@ -632,7 +645,7 @@ __device__ void pass2_chunk(const FusedArgs& A, Smem<K, TM, R, NW, DR, NM>& S, i
 
   const bool valid = c < count;
   int atom = -1, j = 0;
-  double dx = 1.0, dy = 0.0, dz = 0.0, r = 1.0;
+  double dx = 1.0, dy = 0.0, dz = 0.0;  // minimum image in float64, kept for the virial
   if (valid) {
     const int e = start + c;
     j = S.pair_j[e];
@@ -640,13 +653,14 @@ __device__ void pass2_chunk(const FusedArgs& A, Smem<K, TM, R, NW, DR, NM>& S, i
     dx = fold(in.pp.x - S.tpos[atom][0], A.box[0], A.inv_box[0]);
     dy = fold(in.pp.y - S.tpos[atom][1], A.box[1], A.inv_box[1]);
     dz = fold(in.pp.z - S.tpos[atom][2], A.box[2], A.inv_box[2]);
-    r = sqrt(dx * dx + dy * dy + dz * dz);
   }
-  const double ir = 1.0 / r;
-  const double ux = dx * ir, uy = dy * ir, uz = dz * ir;
-  const double arg = r * A.pi_rc;
-  const R fc = valid ? R(0.5 * (1.0 + cos(arg))) : R(0);
-  const R dfc = valid ? R(-0.5 * A.pi_rc * sin(arg)) : R(0);
+  const R rx = R(dx), ry = R(dy), rz = R(dz);
+  const R r = vsqrt(rx * rx + ry * ry + rz * rz);
+  const R ir = vrcp(r);
+  const R ux = rx * ir, uy = ry * ir, uz = rz * ir;
+  const R arg = r * R(A.pi_rc);
+  const R fc = valid ? R(0.5) * (R(1) + vcos(arg)) : R(0);
+  const R dfc = valid ? R(-0.5) * R(A.pi_rc) * vsin(arg) : R(0);
 
   // (W m) and (W dm) for this column's own centre atom, one 16-row tile of
   // the angular features at a time
@@ -678,7 +692,7 @@ __device__ void pass2_chunk(const FusedArgs& A, Smem<K, TM, R, NW, DR, NM>& S, i
   // this pair, accumulated monomial by monomial so that each monomial and
   // its gradient are live only for their own step
   R mono[NM], gx[NM], gy[NM], gz[NM];
-  monomials_n<NM, true>(R(ux), R(uy), R(uz), mono, gx, gy, gz);
+  monomials_n<NM, true>(ux, uy, uz, mono, gx, gy, gz);
   R fv[NA][4], fgx[NA][4], fgy[NA][4], fgz[NA][4];
 #pragma unroll
   for (int ta = 0; ta < NA; ++ta)
@@ -715,12 +729,11 @@ __device__ void pass2_chunk(const FusedArgs& A, Smem<K, TM, R, NW, DR, NM>& S, i
     ty += __shfl_xor(ty, o, 64);
     tz += __shfl_xor(tz, o, 64);
   }
-  // f = s u + (I - u u^T) t / r  (Eq. 10, reassociated), in float64
-  const double sd = s, txd = tx, tyd = ty, tzd = tz;
-  const double ut = ux * txd + uy * tyd + uz * tzd;
-  const double fx = sd * ux + (txd - ut * ux) * ir;
-  const double fy = sd * uy + (tyd - ut * uy) * ir;
-  const double fz = sd * uz + (tzd - ut * uz) * ir;
+  // f = s u + (I - u u^T) t / r  (Eq. 10, reassociated), accumulated in float64
+  const R ut = ux * tx + uy * ty + uz * tz;
+  const double fx = double(s * ux + (tx - ut * ux) * ir);
+  const double fy = double(s * uy + (ty - ut * uy) * ir);
+  const double fz = double(s * uz + (tz - ut * uz) * ir);
   if (valid) {
     if (g == 0) {
       atomicAdd(&A.forces[3 * (long long)j], -fx);
