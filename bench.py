@@ -298,9 +298,10 @@ def main() -> int:
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--precision", type=int, choices=(64, 32), default=64,
                     help="network arithmetic: 64 (float64) or 32 (float32 network, float64 geometry and sums)")
-    ap.add_argument("--fusion", choices=("cached", "recompute", "partial"), default="cached",
+    ap.add_argument("--fusion", choices=("cached", "recompute", "partial", "unfused"), default="cached",
                     help="fusion configuration: one kernel caching the encoder output (default), one kernel "
-                         "recomputing it, or three kernels with the descriptor in HBM")
+                         "recomputing it, three kernels with the descriptor in HBM, or ten kernels (one per "
+                         "equation) with every intermediate in HBM")
     ap.add_argument("--hp", default="",
                     help="comma-separated hyper-parameter overrides, e.g. k=64,lmax=2,enc_cond=1")
     ap.add_argument("--rebuild-every", type=int, default=10)
@@ -361,7 +362,7 @@ def main() -> int:
     ref = pos.clone()
     stream = torch.cuda.current_stream()
     pot = Potential(w.hp, w.weights, stream=stream)
-    pot.set_fusion({"cached": 0, "recompute": 1, "partial": 2}[args.fusion])
+    pot.set_fusion({"cached": 0, "recompute": 1, "partial": 2, "unfused": 3}[args.fusion])
     pot.set_masses(w.masses)
     t0 = time.perf_counter()
     pot.build_neighbors(pos, types, w.box)
@@ -446,8 +447,11 @@ def main() -> int:
         "roofline": {"bound": "mfma", "achieved": achieved, "peak": PEAK_TFLOPS[args.precision], "unit": "TFLOP/s",
                      "frac": achieved / PEAK_TFLOPS[args.precision],
                      "traffic": measured_traffic(w.description, N, args.precision) if args.fusion == "cached" else None,
-                     "kernel": "fused energy/force/virial (k_fused)" if args.fusion != "partial" else
-                               "encoding + regression + derivation kernels (k_fused modes 2-4)",
+                     "kernel": {"cached": "fused energy/force/virial (k_fused)",
+                                "recompute": "fused energy/force/virial (k_fused)",
+                                "partial": "encoding + regression + derivation kernels (k_fused modes 2-4)",
+                                "unfused": "ten kernels, one per equation (setup, radial, angular, moment, "
+                                           "descriptor, regression, adjoint, U, V, force)"}[args.fusion],
                      "kernel_ms": ms_compute,
                      "algorithmic_flop_per_launch": flop},
         "hbm_bytes_per_atom": bpa,

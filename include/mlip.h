@@ -175,7 +175,7 @@ mlip_status mlip_get_neighbors(mlip_ctx* ctx, int64_t* offsets_host, int32_t* id
 
 /*
  * Fusion configuration of mlip_compute (Section 3.4, Table "Configurable
- * fusion"); all three give the same results up to rounding.
+ * fusion"); all four give the same results up to rounding.
  *   MLIP_FUSION_CACHED     one kernel: pass 1 keeps the encoder output and its
  *                          radial derivative per pair in a fixed-size
  *                          per-work-group workspace until pass 2 (default)
@@ -186,17 +186,31 @@ mlip_status mlip_get_neighbors(mlip_ctx* ctx, int64_t* offsets_host, int32_t* id
  *                          paper's partial fusion): G_i and then dE/dG_i go
  *                          through HBM, (l_max+1) k values per atom, which the
  *                          context allocates at the next mlip_compute
+ *   MLIP_FUSION_UNFUSED    ten kernels, one per equation of Eqs. 1-10 (the
+ *                          table's "before fusion" row): every intermediate
+ *                          goes through HBM, per listed neighbour-list entry
+ *                          the pair vector and distance, g_rad and dg_rad/dr,
+ *                          g_ang and its Jacobian, and the U and V rows
+ *                          (4 float64 + 176 values at k = 32), per atom P_i,
+ *                          W_i and G_i / dE/dG_i (1152 values at k = 32,
+ *                          l_max = 3); allocated at the next mlip_compute
+ *                          (MLIP_E_OOM if they do not fit)
+ * Values are float64 or float32 as set by mlip_hparams.precision.
  */
 typedef enum {
   MLIP_FUSION_CACHED = 0,
   MLIP_FUSION_RECOMPUTE = 1,
-  MLIP_FUSION_PARTIAL = 2
+  MLIP_FUSION_PARTIAL = 2,
+  MLIP_FUSION_UNFUSED = 3
 } mlip_fusion;
 
 /*
  * Select the fusion configuration for later mlip_compute calls.  The
- * configurations other than MLIP_FUSION_CACHED exist for k = 32.
- * Errors: MLIP_E_ARG (unknown value, or k != 32 for a non-default one).
+ * configurations other than MLIP_FUSION_CACHED exist for k = 32 with the
+ * irreducible basis and l_max <= 3.  Synchronises the stream and releases
+ * the buffers of a configuration that is left.
+ * Errors: MLIP_E_ARG (unknown value, or a non-default one with other
+ * hyper-parameters), MLIP_E_HIP.
  */
 mlip_status mlip_set_fusion(mlip_ctx* ctx, int32_t fusion);
 

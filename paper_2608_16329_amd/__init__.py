@@ -55,7 +55,7 @@ class Potential:
                                     forces.data_ptr(), virial.data_ptr() if virial is not None else None, totals)
 
     def set_fusion(self, fusion: int) -> None:
-        """binding.MLIP_FUSION_CACHED (default), _RECOMPUTE or _PARTIAL."""
+        """binding.MLIP_FUSION_CACHED (default), _RECOMPUTE, _PARTIAL or _UNFUSED."""
         binding.mlip_set_fusion(self.ctx, fusion)
 
     def neighbors(self):

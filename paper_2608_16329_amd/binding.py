@@ -26,7 +26,7 @@ EXPORTED = ["mlip_weight_count", "mlip_create", "mlip_build_neighbors", "mlip_co
             "mlip_memory_bytes", "mlip_get_stats", "mlip_last_error", "mlip_destroy", "mlip_md_set_masses",
             "mlip_md_first_half", "mlip_md_second_half", "mlip_md_kinetic", "mlip_set_fusion"]
 
-MLIP_FUSION_CACHED, MLIP_FUSION_RECOMPUTE, MLIP_FUSION_PARTIAL = 0, 1, 2
+MLIP_FUSION_CACHED, MLIP_FUSION_RECOMPUTE, MLIP_FUSION_PARTIAL, MLIP_FUSION_UNFUSED = 0, 1, 2, 3
 
 
 class mlip_hparams(ctypes.Structure):

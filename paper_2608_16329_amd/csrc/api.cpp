@@ -143,6 +143,81 @@ std::vector<double> transpose(const double* M, int rows, int cols) {
   return t;
 }
 
+// Copy the totals to the host when asked (synchronising the stream).
+mlip_status finish_compute(mlip_ctx* ctx, double* totals_host) {
+  if (totals_host) {
+    MLIP_HIP(ctx, hipMemcpyAsync(totals_host, ctx->d_totals, 10 * sizeof(double), hipMemcpyDeviceToHost, ctx->stream));
+    MLIP_HIP(ctx, hipStreamSynchronize(ctx->stream));
+  }
+  return MLIP_OK;
+}
+
+// The unfused configuration: ten kernels, one per equation, with the
+// per-entry and per-atom intermediates carved out of one device buffer
+// (each 256-byte aligned).  a is the fused kernel's argument block with the
+// descriptor buffer set.
+mlip_status compute_unfused(mlip_ctx* ctx, FusedArgs& a) {
+  hipStream_t s = ctx->stream;
+  const size_t eb = ctx->elem_bytes, E = size_t(ctx->n_listed), n = size_t(ctx->n);
+  const size_t k = size_t(ctx->hp.k), D = kAngRows;
+  auto al = [](size_t b) { return (b + 255) / 256 * 256; };
+  const size_t sz[9] = {al(4 * sizeof(double) * E), al(k * eb * E), al(k * eb * E), al(D * eb * E),
+                        al(3 * D * eb * E), al(D * k * eb * n), al(D * k * eb * n), al(k * eb * E),
+                        al(D * eb * E)};
+  size_t total = 0;
+  for (size_t b : sz) total += b;
+  MLIP_TRY(ensure(ctx, &ctx->d_unf, &ctx->cap_unf, total, "unfused intermediates"));
+  unsigned char* p[9];
+  size_t off = 0;
+  for (int i = 0; i < 9; ++i) {
+    p[i] = ctx->d_unf + off;
+    off += sz[i];
+  }
+  UnfusedArgs u{};
+  u.pos = a.pos;
+  u.perm = ctx->d_perm;
+  u.offsets = ctx->d_offsets;
+  u.idx = ctx->d_idx;
+  u.qc = ctx->d_qc;
+  u.geo = reinterpret_cast<double*>(p[0]);
+  u.grad = p[1];
+  u.gprime = p[2];
+  u.gang = p[3];
+  u.jang = p[4];
+  u.P = p[5];
+  u.W = p[6];
+  u.U = p[7];
+  u.V = p[8];
+  u.G = ctx->d_gbuf;
+  u.forces = a.forces;
+  u.virial = a.virial;
+  u.totals = ctx->d_totals;
+  for (int d = 0; d < 3; ++d) {
+    u.box[d] = a.box[d];
+    u.inv_box[d] = a.inv_box[d];
+  }
+  u.rc2 = a.rc2;
+  for (int l = 0; l < 8; ++l) u.lrow[l] = a.lrow[l];
+  u.lmax = ctx->hp.lmax;
+  u.n = ctx->n;
+  u.n_entries = ctx->n_listed;
+  a.geo = u.geo;
+  a.grad = p[1];
+  a.gprime = p[2];
+  const int kk = ctx->hp.k, prec = ctx->hp.precision;
+  MLIP_HIP(ctx, launch_unfused(kUnfSetup, prec, u, s));                         // Eq. 1
+  MLIP_HIP(ctx, launch_fused(kk, prec, ctx->acfg, kModeRadial, a, ctx->n_blocks, s));  // Eq. 2
+  MLIP_HIP(ctx, launch_unfused(kUnfAngular, prec, u, s));                       // Eq. 3
+  MLIP_HIP(ctx, launch_unfused(kUnfMoment, prec, u, s));                        // Eq. 4
+  MLIP_HIP(ctx, launch_unfused(kUnfDescriptor, prec, u, s));                    // Eq. 5
+  MLIP_HIP(ctx, launch_fused(kk, prec, ctx->acfg, kModeRegress, a, ctx->n_blocks, s));  // Eq. 6
+  MLIP_HIP(ctx, launch_unfused(kUnfAdjoint, prec, u, s));                       // Eq. 7
+  MLIP_HIP(ctx, launch_unfused(kUnfU, prec, u, s));                             // Eq. 8
+  MLIP_HIP(ctx, launch_unfused(kUnfV, prec, u, s));                             // Eq. 9
+  MLIP_HIP(ctx, launch_unfused(kUnfForce, prec, u, s));                         // Eq. 10
+  return MLIP_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -437,10 +512,14 @@ mlip_status mlip_compute(mlip_ctx* ctx, const double* pos_dev, double* energy_de
     a.tile_start[sp_i] = t;
     if (sp_i < a.C) t += (ctx->species_start[sp_i + 1] - ctx->species_start[sp_i] + ctx->tile_atoms - 1) / ctx->tile_atoms;
   }
-  if (ctx->fusion == MLIP_FUSION_PARTIAL) {
+  if (ctx->fusion == MLIP_FUSION_PARTIAL || ctx->fusion == MLIP_FUSION_UNFUSED) {
     const size_t need = size_t(n) * size_t((ctx->hp.lmax + 1) * ctx->hp.k) * ctx->elem_bytes;
     MLIP_TRY(ensure(ctx, &ctx->d_gbuf, &ctx->cap_gbuf, need, "descriptor buffer"));
     a.gbuf = ctx->d_gbuf;
+  }
+  if (ctx->fusion == MLIP_FUSION_UNFUSED && ctx->n_tiles > 0) {
+    MLIP_TRY(compute_unfused(ctx, a));
+    return finish_compute(ctx, totals_host);
   }
   if (ctx->n_tiles > 0) {
     const int k = ctx->hp.k, prec = ctx->hp.precision;
@@ -452,11 +531,7 @@ mlip_status mlip_compute(mlip_ctx* ctx, const double* pos_dev, double* energy_de
       MLIP_HIP(ctx, launch_fused(k, prec, ctx->acfg, ctx->fusion == MLIP_FUSION_RECOMPUTE ? 1 : 0, a, ctx->n_blocks, s));
     }
   }
-  if (totals_host) {
-    MLIP_HIP(ctx, hipMemcpyAsync(totals_host, ctx->d_totals, 10 * sizeof(double), hipMemcpyDeviceToHost, s));
-    MLIP_HIP(ctx, hipStreamSynchronize(s));
-  }
-  return MLIP_OK;
+  return finish_compute(ctx, totals_host);
 }
 
 mlip_status mlip_get_neighbors(mlip_ctx* ctx, int64_t* offsets_host, int32_t* idx_host) {
@@ -490,12 +565,23 @@ mlip_status mlip_get_neighbors(mlip_ctx* ctx, int64_t* offsets_host, int32_t* id
 mlip_status mlip_set_fusion(mlip_ctx* ctx, int32_t fusion) {
   if (!ctx) return MLIP_E_ARG;
   ctx->err.clear();
-  if (fusion != MLIP_FUSION_CACHED && fusion != MLIP_FUSION_RECOMPUTE && fusion != MLIP_FUSION_PARTIAL)
+  if (fusion != MLIP_FUSION_CACHED && fusion != MLIP_FUSION_RECOMPUTE && fusion != MLIP_FUSION_PARTIAL &&
+      fusion != MLIP_FUSION_UNFUSED)
     return fail(ctx, MLIP_E_ARG, "unknown fusion configuration");
   if (fusion != MLIP_FUSION_CACHED && (ctx->hp.k != 32 || ctx->acfg != 0))
     return fail(ctx, MLIP_E_ARG,
-                "the recompute and three-kernel configurations exist for k = 32 and the irreducible basis "
-                "with l_max <= 3 only");
+                "the recompute, three-kernel and unfused configurations exist for k = 32 and the irreducible "
+                "basis with l_max <= 3 only");
+  // buffers of a configuration that is left are released
+  MLIP_HIP(ctx, hipStreamSynchronize(ctx->stream));
+  if (fusion != MLIP_FUSION_UNFUSED) {
+    release(ctx, &ctx->d_unf, ctx->cap_unf);
+    ctx->cap_unf = 0;
+  }
+  if (fusion != MLIP_FUSION_PARTIAL && fusion != MLIP_FUSION_UNFUSED) {
+    release(ctx, &ctx->d_gbuf, ctx->cap_gbuf);
+    ctx->cap_gbuf = 0;
+  }
   ctx->fusion = fusion;
   return MLIP_OK;
 }
@@ -538,7 +624,7 @@ void mlip_destroy(mlip_ctx* ctx) {
   void* bufs[] = {ctx->d_enc, ctx->d_head, ctx->d_qc, ctx->d_inv_mass, ctx->d_types, ctx->d_perm,
                   ctx->d_key, ctx->d_spos, ctx->d_rowcnt, ctx->d_offsets, ctx->d_idx, ctx->d_cell_count,
                   ctx->d_cell_start, ctx->d_scan_tmp, ctx->d_ws, ctx->d_totals, ctx->d_counters,
-                  ctx->d_flags, ctx->d_reduce, ctx->d_gbuf};
+                  ctx->d_flags, ctx->d_reduce, ctx->d_gbuf, ctx->d_unf};
   for (void* p : bufs)
     if (p) (void)hipFree(p);
   (void)hipGetLastError();

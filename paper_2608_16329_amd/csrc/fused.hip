@@ -40,6 +40,7 @@
 // later product as B (contracting over its rows; k-step q covers rows
 // drow(q, 0..3)) or as A (X^T, same contraction); the host packs weight
 // fragments with the same row map.
+#include "kernel_math.h"
 #include "mlip_internal.h"
 
 namespace mlip {
@@ -134,8 +135,6 @@ __device__ __forceinline__ float sigmoid(float z) {
   return __builtin_amdgcn_rcpf(1.0f + e);
 }
 
-__device__ __forceinline__ double fold(double d, double L, double invL) { return d - L * rint(d * invL); }
-
 // Pair geometry after the minimum-image difference (which stays in float64):
 // IEEE float64 operations, or the float32 hardware instructions (about one
 // ulp; sine and cosine take revolutions, valid here since 0 <= x <= pi).
@@ -147,43 +146,6 @@ __device__ __forceinline__ double vcos(double x) { return cos(x); }
 __device__ __forceinline__ float vcos(float x) { return __builtin_amdgcn_cosf(x * 0.159154943f); }
 __device__ __forceinline__ double vsin(double x) { return sin(x); }
 __device__ __forceinline__ float vsin(float x) { return __builtin_amdgcn_sinf(x * 0.159154943f); }
-
-// Cartesian monomials of degree <= 3 in the order of the angular table.
-template <typename R>
-__device__ __forceinline__ void monomials(R x, R y, R z, R m[kMonomials]) {
-  m[0] = R(1);
-  m[1] = x; m[2] = y; m[3] = z;
-  m[4] = x * x; m[5] = x * y; m[6] = x * z; m[7] = y * y; m[8] = y * z; m[9] = z * z;
-  m[10] = x * x * x; m[11] = x * x * y; m[12] = x * x * z; m[13] = x * y * y; m[14] = x * y * z;
-  m[15] = x * z * z; m[16] = y * y * y; m[17] = y * y * z; m[18] = y * z * z; m[19] = z * z * z;
-}
-
-// Gradients of the monomials with respect to (x, y, z).
-template <typename R>
-__device__ __forceinline__ void monomial_grads(R x, R y, R z, R gx[kMonomials], R gy[kMonomials],
-                                               R gz[kMonomials]) {
-  const R xx = x * x, yy = y * y, zz = z * z;
-  gx[0] = 0; gy[0] = 0; gz[0] = 0;
-  gx[1] = 1; gy[1] = 0; gz[1] = 0;
-  gx[2] = 0; gy[2] = 1; gz[2] = 0;
-  gx[3] = 0; gy[3] = 0; gz[3] = 1;
-  gx[4] = 2 * x; gy[4] = 0; gz[4] = 0;
-  gx[5] = y; gy[5] = x; gz[5] = 0;
-  gx[6] = z; gy[6] = 0; gz[6] = x;
-  gx[7] = 0; gy[7] = 2 * y; gz[7] = 0;
-  gx[8] = 0; gy[8] = z; gz[8] = y;
-  gx[9] = 0; gy[9] = 0; gz[9] = 2 * z;
-  gx[10] = 3 * xx; gy[10] = 0; gz[10] = 0;
-  gx[11] = 2 * x * y; gy[11] = xx; gz[11] = 0;
-  gx[12] = 2 * x * z; gy[12] = 0; gz[12] = xx;
-  gx[13] = yy; gy[13] = 2 * x * y; gz[13] = 0;
-  gx[14] = y * z; gy[14] = x * z; gz[14] = x * y;
-  gx[15] = zz; gy[15] = 0; gz[15] = 2 * x * z;
-  gx[16] = 0; gy[16] = 3 * yy; gz[16] = 0;
-  gx[17] = 0; gy[17] = 2 * y * z; gz[17] = yy;
-  gx[18] = 0; gy[18] = zz; gz[18] = 2 * y * z;
-  gx[19] = 0; gy[19] = 0; gz[19] = 3 * zz;
-}
 
 // Exponents (a, b, c) of the Cartesian monomials of degree <= 5, degree by
 // degree and lexicographic with x first within a degree (the column order of
@@ -758,6 +720,39 @@ __device__ void pass2_chunk(const FusedArgs& A, Smem<K, TM, R, NW, DR, NM>& S, i
   }
 }
 
+// Radial kernel of the unfused configuration (Eq. 2 as a kernel of its own)
+// on one chunk: g = fc(r) MLP(r) and dg/dr of each pair from the distance
+// the setup kernel stored for its neighbour-list entry, written back by
+// entry.  The chunk's pair slots hold entry indices relative to the tile's
+// first entry.
+template <int K, int TM, typename R, int NW, int DR, int NM>
+__device__ void radial_chunk(const FusedArgs& A, const Smem<K, TM, R, NW, DR, NM>& S, int ch) {
+  constexpr int KT = K / 16;
+  const int lane = threadIdx.x & 63, g = lane >> 4, c = lane & 15;
+  const bool valid = c < S.ch_count[ch];
+  const long long e = S.row_beg[0] + (valid ? S.pair_j[S.ch_start[ch] + c] : 0);
+  const R r = valid ? R(A.geo[4 * e + 3]) : R(1);
+  const R arg = r * R(A.pi_rc);
+  const R fc = valid ? R(0.5) * (R(1) + vcos(arg)) : R(0);
+  const R dfc = valid ? R(-0.5) * R(A.pi_rc) * vsin(arg) : R(0);
+  R h[8][4], dh[8][4];
+  const R* __restrict__ layer = encoder_hidden(A, S, S.ch_s[ch], r, chunk_table(A, S, ch), h, dh);
+  R mB[KT][4], dmB[KT][4];
+  encoder_out_cols<K, R>(layer, h, dh, mB, dmB);
+  if (valid) {
+    R* __restrict__ gr = static_cast<R*>(A.grad) + e * K;
+    R* __restrict__ gp = static_cast<R*>(A.gprime) + e * K;
+#pragma unroll
+    for (int Tc = 0; Tc < KT; ++Tc)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int col = 16 * Tc + drow<R>(q, g);
+        gr[col] = fc * mB[Tc][q];
+        gp[col] = dfc * mB[Tc][q] + fc * dmB[Tc][q];
+      }
+  }
+}
+
 // Descriptor value x[in] = vec(G)[in] of tile atom a (Eq. 5): the l = 0
 // block is linear, a block l >= 1 (angular rows lrow[l] .. lrow[l+1]-1) is
 // the quadratic form sum_m rw[m] P[m][col]^2 with the block's diagonal
@@ -985,12 +980,14 @@ __device__ __forceinline__ void stage_first_layer(const FusedArgs& A, Smem<K, TM
   }
 }
 
-// What one launch does (Section 3.4 fusion configurations, numbered as in
-// mlip_fusion): the single kernel that caches (m, dm) between its two
-// passes or recomputes them in pass 2, or one of the three kernels of the
-// partial configuration: encoding (Eqs. 1-5, G to HBM), regression (Eq. 6,
-// E and dE/dG to HBM) and derivation (Eqs. 7-10, recomputing P).
-enum Mode { kCached = 0, kRecompute = 1, kEncode = 2, kRegress = 3, kDerive = 4 };
+// What one launch does (Section 3.4 fusion configurations): the single
+// kernel that caches (m, dm) between its two passes or recomputes them in
+// pass 2; one of the three kernels of the partial configuration: encoding
+// (Eqs. 1-5, G to HBM), regression (Eq. 6, E and dE/dG to HBM) and
+// derivation (Eqs. 7-10, recomputing P); or the radial kernel of the unfused
+// configuration (Eq. 2 alone, which uses the regression kernel as well).
+enum Mode { kCached = 0, kRecompute = 1, kEncode = 2, kRegress = 3, kDerive = 4, kRadial = 5 };
+static_assert(kRegress == kModeRegress && kRadial == kModeRadial, "mode numbers of the unfused configuration");
 
 template <int K, int TM, typename R, int NW, int DR, int NM, int MODE>
 __global__ __launch_bounds__(64 * NW, 1) void k_fused(FusedArgs A) {
@@ -1054,7 +1051,8 @@ __global__ __launch_bounds__(64 * NW, 1) void k_fused(FusedArgs A) {
       if (tid == 0) S.row_beg[0] = A.offsets[a0];
     }
     for (int u = tid; u < kMaxSpecies * TM; u += (64 * NW)) S.cnt[u / TM][u % TM] = 0;
-    for (int u = tid; u < TM * DR * (K + 1); u += (64 * NW)) (&S.P[0][0][0])[u] = R(0);
+    if constexpr (MODE != kRadial)
+      for (int u = tid; u < TM * DR * (K + 1); u += (64 * NW)) (&S.P[0][0][0])[u] = R(0);
     __syncthreads();
     const int nent = S.ent_base[na];
     const long long ebase = S.row_beg[0];
@@ -1075,10 +1073,17 @@ __global__ __launch_bounds__(64 * NW, 1) void k_fused(FusedArgs A) {
         es[k] = -1;
         const int j = ej[k];
         if (j >= 0) {
-          const double dx = fold(A.pos[3 * (long long)j] - S.tpos[a][0], A.box[0], A.inv_box[0]);
-          const double dy = fold(A.pos[3 * (long long)j + 1] - S.tpos[a][1], A.box[1], A.inv_box[1]);
-          const double dz = fold(A.pos[3 * (long long)j + 2] - S.tpos[a][2], A.box[2], A.inv_box[2]);
-          if (dx * dx + dy * dy + dz * dz < A.rc2) {
+          bool active;
+          if constexpr (MODE == kRadial) {
+            // the setup kernel marked entries beyond the cutoff
+            active = A.geo[4 * (ebase + e) + 3] >= 0.0;
+          } else {
+            const double dx = fold(A.pos[3 * (long long)j] - S.tpos[a][0], A.box[0], A.inv_box[0]);
+            const double dy = fold(A.pos[3 * (long long)j + 1] - S.tpos[a][1], A.box[1], A.inv_box[1]);
+            const double dz = fold(A.pos[3 * (long long)j + 2] - S.tpos[a][2], A.box[2], A.inv_box[2]);
+            active = dx * dx + dy * dy + dz * dz < A.rc2;
+          }
+          if (active) {
             es[k] = A.types[j];
             atomicAdd(&S.cnt[es[k]][a], 1);
             ++my_active;
@@ -1141,7 +1146,7 @@ __global__ __launch_bounds__(64 * NW, 1) void k_fused(FusedArgs A) {
         // the list builder groups every row by species, so p always lies in
         // the (species, atom) run; the bound only keeps LDS accesses in range
         if (p >= 0 && p < S.n_active) {
-          S.pair_j[p] = ej[k];
+          S.pair_j[p] = MODE == kRadial ? tid * kPer + k : ej[k];
           S.pair_a[p] = (unsigned char)a;
         }
         ++prefix;
@@ -1151,7 +1156,17 @@ __global__ __launch_bounds__(64 * NW, 1) void k_fused(FusedArgs A) {
 
     // ---- B: pass 1 ---------------------------------------------------------
     nch = S.n_chunks;
-    {
+    if constexpr (MODE == kRadial) {
+      int ch = wave;
+      while (ch < nch) {
+        const int ch2 = grab_chunk(&S.next_chunk[0]);
+        radial_chunk<K, TM, R, NW, DR, NM>(A, S, ch);
+        ch = ch2;
+      }
+      if (tid == 0) atomicAdd(&A.counters[0], (unsigned long long)S.n_active);
+      __syncthreads();
+      continue;
+    } else {
       constexpr bool kWs = MODE == kCached || MODE == kDerive;
       int ch = wave;
       PairPos next = ch < nch ? load_pair_pos(A, S, ch) : PairPos{0.0, 0.0, 0.0};
@@ -1171,7 +1186,7 @@ __global__ __launch_bounds__(64 * NW, 1) void k_fused(FusedArgs A) {
       head_stage<K, TM, R, NW, DR, NM, false>(A, S);
     } else if constexpr (MODE == kRegress) {
       head_stage<K, TM, R, NW, DR, NM, true>(A, S);
-    } else {
+    } else if constexpr (MODE == kEncode || MODE == kDerive) {
       // encoding kernel: G to HBM; derivation kernel: W from dE/dG in HBM
       const int nin = (A.lmax + 1) * K;
       R* __restrict__ gbuf = static_cast<R*>(A.gbuf) + (long long)a0 * nin;
@@ -1278,6 +1293,7 @@ hipError_t launch_mode(int mode, const FusedArgs& a, int n_blocks, hipStream_t s
     case kEncode: return launch_k<K, TM, R, NW, DR, NM, kEncode>(a, n_blocks, s);
     case kRegress: return launch_k<K, TM, R, NW, DR, NM, kRegress>(a, n_blocks, s);
     case kDerive: return launch_k<K, TM, R, NW, DR, NM, kDerive>(a, n_blocks, s);
+    case kRadial: return launch_k<K, TM, R, NW, DR, NM, kRadial>(a, n_blocks, s);
     default: return hipErrorInvalidValue;
   }
 }

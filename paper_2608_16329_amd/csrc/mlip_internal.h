@@ -57,7 +57,13 @@ struct FusedArgs {
   unsigned long long* counters;  // [0] active pairs (zeroed before launch)
   void* ws;                   // per-block workspace
   long long ws_slot;          // values per block slot
-  void* gbuf;                 // [n][(lmax+1) k] by sorted slot: G, then dE/dG (three-kernel configuration)
+  void* gbuf;                 // [n][(lmax+1) k] by sorted slot: G, then dE/dG (three-kernel and unfused configurations)
+  // unfused configuration, radial kernel: per neighbour-list entry the pair
+  // vector and distance written by the setup kernel, and the radial features
+  // and their r-derivatives it writes
+  const double* geo;          // [entries][4]: dx, dy, dz, r (r = -1 beyond the cutoff)
+  void* grad;                 // [entries][k]
+  void* gprime;               // [entries][k]
   double box[3];
   double inv_box[3];
   double rc, rc2;
@@ -69,6 +75,38 @@ struct FusedArgs {
   int n_tiles;
   int species_start[kMaxSpecies + 1];  // first sorted slot of each species
   int tile_start[kMaxSpecies + 1];     // first tile of each species
+};
+
+// Arguments of the kernels of the unfused configuration (one kernel per
+// equation, every intermediate in HBM).  Per-entry arrays are indexed by the
+// neighbour-list entry (rows in sorted order), per-atom arrays by sorted
+// slot; the network-side arrays hold the arithmetic type (precision).
+struct UnfusedArgs {
+  const double* pos;          // caller order [n][3]
+  const int32_t* perm;        // sorted slot -> caller index
+  const int64_t* offsets;     // [n+1]
+  const int32_t* idx;         // neighbour entries, caller indices
+  const void* qc;             // angular table [16][20], then the row metric [16]
+  double* geo;                // [entries][4]: dx, dy, dz, r (r = -1 beyond the cutoff)
+  const void* grad;           // [entries][k]  g_rad (written by the radial kernel)
+  const void* gprime;         // [entries][k]  dg_rad/dr
+  void* gang;                 // [entries][16] g_ang
+  void* jang;                 // [entries][16][3] dg_ang/dr_ij
+  void* P;                    // [n][16][k] moment
+  void* G;                    // [n][(lmax+1) k] descriptor, then dE/dG
+  void* W;                    // [n][16][k] dE/dP
+  void* U;                    // [entries][k] dE_i/dg_rad
+  void* V;                    // [entries][16] dE_i/dg_ang
+  double* forces;             // [n][3], zeroed before launch
+  double* virial;             // [n][9] or null
+  double* totals;             // [10] (entries 1..9 accumulated here)
+  double box[3];
+  double inv_box[3];
+  double rc2;
+  int lrow[8];
+  int lmax;
+  long long n;                // atoms
+  long long n_entries;        // listed entries
 };
 
 // Arguments of the neighbour-list kernels.
@@ -144,6 +182,8 @@ struct mlip_ctx {
   int lrow[8] = {0};                // first angular row of each order
   unsigned char* d_gbuf = nullptr;  // G / dE/dG per atom (three-kernel configuration), cap_gbuf bytes
   size_t cap_gbuf = 0;
+  unsigned char* d_unf = nullptr;   // intermediates of the unfused configuration, cap_unf bytes
+  size_t cap_unf = 0;
 };
 
 namespace mlip {
@@ -185,6 +225,14 @@ int angular_config(int angular, int lmax);
 void angular_table_shape(int acfg, int* rows, int* cols);
 int fused_tile_max(int k, int precision, int acfg);  // centre atoms per tile of that instantiation
 hipError_t launch_fused(int k, int precision, int acfg, int mode, const FusedArgs& a, int n_blocks, hipStream_t s);
+// Modes of launch_fused used by the unfused configuration.
+constexpr int kModeRegress = 3;   // Eq. 6: G -> E_i, dE/dG
+constexpr int kModeRadial = 5;    // Eq. 2: distances -> g_rad, dg_rad/dr per entry
+
+// unfused.hip: the other eight kernels of the unfused configuration, in
+// order; k = 32, irreducible basis with l_max <= 3.
+enum UnfusedStage { kUnfSetup, kUnfAngular, kUnfMoment, kUnfDescriptor, kUnfAdjoint, kUnfU, kUnfV, kUnfForce };
+hipError_t launch_unfused(int stage, int precision, const UnfusedArgs& a, hipStream_t s);
 
 // md.hip
 hipError_t launch_md_first_half(double* pos, double* vel, const double* forces, const int32_t* types,

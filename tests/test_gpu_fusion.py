@@ -1,8 +1,9 @@
 """GPU parity of the fusion configurations (Section 3.4, Table "Configurable
 fusion"): the single kernel that recomputes the encoder in its second pass
-(the paper's mega-fusion) and the three-kernel split with G_i and dE/dG_i in
-HBM (the paper's partial fusion), against the oracle and against the default
-cached configuration."""
+(the paper's mega-fusion), the three-kernel split with G_i and dE/dG_i in
+HBM (the paper's partial fusion) and the ten-kernel unfused pipeline with
+every intermediate in HBM (the table's "before fusion" row), against the
+oracle and against the default cached configuration."""
 import dataclasses
 
 import numpy as np
@@ -27,7 +28,7 @@ def _rel(a, ref):
     return max_abs(a, ref) / max(float(np.max(np.abs(ref))), 1e-300)
 
 
-@pytest.mark.parametrize("fusion", [1, 2])
+@pytest.mark.parametrize("fusion", [1, 2, 3])
 @pytest.mark.parametrize("precision", [64, 32])
 @pytest.mark.parametrize("name,n,over", [("fcc-binary-4", None, {}), ("fcc-hea6-128", 5, {}),
                                          ("fcc-binary-4", None, {"lmax": 1, "enc_cond": 0, "reg_cond": 0}),
@@ -55,22 +56,74 @@ def test_fusion_configurations_match_oracle(fusion, precision, name, n, over):
     g["pot"].close()
 
 
-def test_configurations_agree_and_partial_holds_descriptor_memory():
-    """The three configurations on one input agree to rounding; the
-    three-kernel one holds (l_max + 1) k doubles per atom more."""
+def _unfused_bytes(n_atoms, n_listed, k, lmax, eb):
+    """Intermediates of the unfused configuration: per listed entry the pair
+    vector and distance (4 float64), g_rad and dg_rad/dr (2k), g_ang and its
+    Jacobian (16 + 48), U and V rows (k + 16); per atom P and W (2 x 16k) and
+    the descriptor buffer ((l_max + 1) k); each sub-buffer 256-byte aligned."""
+    al = lambda b: (b + 255) // 256 * 256
+    per_entry = [4 * 8, k * eb, k * eb, 16 * eb, 48 * eb, k * eb, 16 * eb]
+    per_atom = [16 * k * eb, 16 * k * eb]
+    return (sum(al(b * n_listed) for b in per_entry) + sum(al(b * n_atoms) for b in per_atom)
+            + n_atoms * (lmax + 1) * k * eb)
+
+
+def test_configurations_agree_and_hold_their_intermediates():
+    """The four configurations on one input agree to rounding; the
+    three-kernel one holds (l_max + 1) k values per atom more, the unfused one
+    every intermediate of Eqs. 1-10."""
     w = synth.make_workload("fcc-hea6-128", seed=3, n=6)
     out = {}
-    for fusion in (0, 1, 2):
+    for fusion in (0, 1, 2, 3):
         out[fusion] = _eval(w.hp, w, fusion)
-    for fusion in (1, 2):
+    for fusion in (1, 2, 3):
         for key in ("E_i", "F", "virial"):
             d = max_abs(out[fusion][key], out[0][key])
             log(f"[fusion] {fusion} vs cached {key}: {d:.2e}")
             assert d <= TOL64
     extra = out[2]["pot"].memory_bytes() - out[0]["pot"].memory_bytes()
     assert extra == len(w.pos) * (w.hp.lmax + 1) * w.hp.k * 8
+    n_listed = out[3]["stats"]["n_listed_pairs"]
+    extra = out[3]["pot"].memory_bytes() - out[0]["pot"].memory_bytes()
+    assert extra == _unfused_bytes(len(w.pos), n_listed, w.hp.k, w.hp.lmax, 8)
     for g in out.values():
         g["pot"].close()
+
+
+def test_unfused_md_steps_and_switching_back():
+    """Ten velocity-Verlet steps in the unfused configuration track the cached
+    configuration; switching a context back releases the intermediates."""
+    import torch
+    from paper_2608_16329_amd import Potential
+    w = synth.make_workload("fcc-binary-4", seed=21)
+    n = len(w.pos)
+    runs = {}
+    for fusion in (0, 3):
+        pot = Potential(w.hp, w.weights)
+        pot.set_fusion(fusion)
+        pot.set_masses(w.masses)
+        pos = torch.from_numpy(w.pos.copy()).to("cuda:0")
+        vel = torch.from_numpy(w.vel.copy()).to("cuda:0")
+        types = torch.from_numpy(w.types).to("cuda:0")
+        F = torch.zeros((n, 3), dtype=torch.float64, device="cuda:0")
+        pot.build_neighbors(pos, types, w.box)
+        pot.compute(pos, F)
+        for _ in range(10):
+            pot.md_first_half(pos, vel, F, w.dt)
+            pot.build_neighbors(pos, types, w.box)
+            pot.compute(pos, F)
+            pot.md_second_half(vel, F, w.dt)
+        torch.cuda.synchronize()
+        runs[fusion] = (pos.cpu().numpy(), F.cpu().numpy())
+        if fusion == 3:
+            held = pot.memory_bytes()
+            pot.set_fusion(0)
+            assert pot.memory_bytes() < held
+        pot.close()
+    dx = max_abs(runs[3][0], runs[0][0])
+    dF = max_abs(runs[3][1], runs[0][1])
+    log(f"[fusion] unfused vs cached after 10 steps: max|dx|={dx:.2e} max|dF|={dF:.2e}")
+    assert dx <= 1e-10 and dF <= 1e-8
 
 
 def test_fusion_argument_checks():
@@ -82,7 +135,8 @@ def test_fusion_argument_checks():
     pot.close()
     hp16 = dataclasses.replace(hp, k=16)
     pot = Potential(hp16, synth.random_weights(hp16, 0))
-    with pytest.raises(MlipError, match="ARG"):
-        pot.set_fusion(2)
+    for fusion in (1, 2, 3):
+        with pytest.raises(MlipError, match="ARG"):
+            pot.set_fusion(fusion)
     pot.set_fusion(0)
     pot.close()
