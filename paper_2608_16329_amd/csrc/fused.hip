@@ -780,14 +780,56 @@ __device__ __forceinline__ void adjoint_from_grad(const FusedArgs& A, Smem<K, TM
   }
 }
 
+// Weight fragments of the head products, consumed in groups of 16 k-steps.
+// Group G of a wavefront that owns output rows (w < 4): the first layer's
+// k-steps 16G .. 16G+15, then the hidden layers forward, the hidden layers
+// backward (A_t^T), then the A0^T output tiles tt = w, w + NW, ...; the
+// other wavefronts only take A0^T tiles.  Element ks of a group is at
+// p[ks * stride * 64]; n is the group's k-step count (0 past the end).
+template <typename R>
+struct HeadGroup {
+  const R* p;
+  int stride, n;
+};
+
+template <typename R>
+__device__ __forceinline__ HeadGroup<R> head_group(int G, bool rw, int w, int nw, int nin, int nhid,
+                                                   const R* __restrict__ A0f, const R* __restrict__ A0Tf,
+                                                   const R* __restrict__ hid) {
+  constexpr int RW = kHeadWidth;
+  constexpr int HS = 2 * RW * RW + RW;
+  const int lane = threadIdx.x & 63;
+  const int tin = nin / 16, k0 = nin / 4, nl0 = (k0 + 15) / 16;
+  if (rw) {
+    if (G < nl0) return {A0f + (64 * G + w) * 64 + lane, 4, k0 - 16 * G < 16 ? k0 - 16 * G : 16};
+    G -= nl0;
+    if (G < nhid) return {hid + G * HS + w * 64 + lane, 4, 16};
+    G -= nhid;
+    if (G < nhid) return {hid + (nhid - 1 - G) * HS + RW * RW + w * 64 + lane, 4, 16};
+    G -= nhid;
+  }
+  const int tt = w + nw * G;
+  if (tt < tin) return {A0Tf + tt * 64 + lane, tin, 16};
+  return {A0Tf, 0, 0};
+}
+
+template <typename R>
+__device__ __forceinline__ void head_load(const HeadGroup<R>& d, R (&f)[16]) {
+#pragma unroll
+  for (int ks = 0; ks < 16; ++ks) f[ks] = ks < d.n ? d.p[ks * d.stride * 64] : R(0);
+}
+
 // Descriptor (Eq. 5), head forward and backward (Eq. 6) and W = dE/dP
 // (Eq. 7) for the tile on MFMA: the tile's atoms are the 16 columns of every
 // product and wavefront w < 4 owns rows 16w..16w+15 of each 64-wide layer.
 // Activations live in LDS feature-major ([feature][atom]) so that B-operand
 // reads are contiguous; pre-activations stay in registers for the backward
-// pass.  With kRegress (the regression kernel of the three-kernel
-// configuration) the descriptor comes from HBM and dE/dx goes back to HBM in
-// its place instead of forming W.
+// pass.  Each wavefront streams its weight fragments one 16-k-step group
+// ahead of the products (the first group before the descriptor is formed),
+// so a layer's fragments arrive while the previous layer and its barriers
+// run.  With kRegress (the regression kernel of the three-kernel and unfused
+// configurations) the descriptor comes from HBM and dE/dx goes back to HBM
+// in its place instead of forming W.
 template <int K, int TM, typename R, int NW, int DR, int NM, bool kRegress>
 __device__ void head_stage(const FusedArgs& A, Smem<K, TM, R, NW, DR, NM>& S) {
   constexpr int RW = kHeadWidth;
@@ -798,6 +840,29 @@ __device__ void head_stage(const FusedArgs& A, Smem<K, TM, R, NW, DR, NM>& S) {
   const int na = S.na;
   const int nin = (A.lmax + 1) * K;
   const int tin = nin / 16;
+  const int nhid = A.reg_hidden - 1;
+  const int rho = A.reg_cond ? S.tile_species : 0;
+  const R* __restrict__ A0f = static_cast<const R*>(A.head) + (long long)rho * A.head_stride;  // A0 fragments
+  const R* __restrict__ A0Tf = A0f + RW * nin;                                               // A0^T fragments
+  const R* __restrict__ c0 = A0Tf + RW * nin;
+  const R* __restrict__ hid = c0 + RW;
+  const R* __restrict__ aout = hid + nhid * HS;
+  // this lane's result rows are 16 w + drow(q, g); with more than 4
+  // wavefronts the others only join the barriers of the row-parallel steps
+  // and take A0^T tiles.  Each weight fragment multiplies the CG column
+  // groups of atoms.
+  const bool rw = w < RW / 16;
+  int G = 0;
+  R fcur[16], fnext[16];
+  head_load(head_group(G, rw, w, NW, nin, nhid, A0f, A0Tf, hid), fnext);
+  // next group: the fetched one becomes current and the one after it is fetched
+#define ADVANCE()                                                          \
+  do {                                                                     \
+    _Pragma("unroll") for (int ks_ = 0; ks_ < 16; ++ks_) fcur[ks_] = fnext[ks_]; \
+    ++G;                                                                   \
+    head_load(head_group(G, rw, w, NW, nin, nhid, A0f, A0Tf, hid), fnext); \
+  } while (0)
+
   R* __restrict__ gbuf = kRegress ? static_cast<R*>(A.gbuf) + (long long)S.a0 * nin : nullptr;
   for (int u = tid; u < NC * nin; u += (64 * NW)) {
     const int a = u % NC, in = u / NC;
@@ -807,41 +872,34 @@ __device__ void head_stage(const FusedArgs& A, Smem<K, TM, R, NW, DR, NM>& S) {
   }
   __syncthreads();
 
-  const int rho = A.reg_cond ? S.tile_species : 0;
-  const R* __restrict__ A0f = static_cast<const R*>(A.head) + (long long)rho * A.head_stride;  // A0 fragments
-  const R* __restrict__ A0Tf = A0f + RW * nin;                                               // A0^T fragments
-  const R* __restrict__ c0 = A0Tf + RW * nin;
-  const R* __restrict__ hid = c0 + RW;
-  const R* __restrict__ aout = hid + (A.reg_hidden - 1) * HS;
-  // this lane's result rows are 16 w + drow(q, g); with more than 4
-  // wavefronts the others only join the barriers of the row-parallel steps.
-  // Each weight fragment multiplies the CG column groups of atoms.
-  const bool rw = w < RW / 16;
 #define ROW(q) (16 * w + drow<R>(q, g))
 
-  // layer 0: z0 = A0 x + c0
+  // layer 0: z0 = A0 x + c0, over nin / 4 k-steps in groups of 16 with two
+  // accumulators alternating
   v4<R> z0[CG];
 #pragma unroll
   for (int cg = 0; cg < CG; ++cg) z0[cg] = v4<R>{0, 0, 0, 0};
   if (rw) {
-    // nin / 4 k-steps, a multiple of 4: fragments of 4 k-steps are loaded
-    // together and two accumulators alternate
     v4<R> z0b[CG];
 #pragma unroll
     for (int cg = 0; cg < CG; ++cg) {
       z0[cg] = v4<R>{c0[ROW(0)], c0[ROW(1)], c0[ROW(2)], c0[ROW(3)]};
       z0b[cg] = v4<R>{0, 0, 0, 0};
     }
-    for (int k4 = 0; k4 < nin / 16; ++k4) {
-      R fa[4];
+    const int k0 = nin / 4;
+    for (int kb = 0; kb < k0; kb += 16) {
+      ADVANCE();
 #pragma unroll
-      for (int i = 0; i < 4; ++i) fa[i] = A0f[((4 * k4 + i) * 4 + w) * 64 + lane];
+      for (int ks = 0; ks < 16; ks += 2) {
+        if (kb + ks < k0) {
+          const int k = kb + ks;
 #pragma unroll
-      for (int cg = 0; cg < CG; ++cg) {
-        z0[cg] = mfma(fa[0], S.u.hd.xT[16 * k4 + drow<R>(0, g)][16 * cg + c], z0[cg]);
-        z0b[cg] = mfma(fa[1], S.u.hd.xT[16 * k4 + drow<R>(1, g)][16 * cg + c], z0b[cg]);
-        z0[cg] = mfma(fa[2], S.u.hd.xT[16 * k4 + drow<R>(2, g)][16 * cg + c], z0[cg]);
-        z0b[cg] = mfma(fa[3], S.u.hd.xT[16 * k4 + drow<R>(3, g)][16 * cg + c], z0b[cg]);
+          for (int cg = 0; cg < CG; ++cg) {
+            z0[cg] = mfma(fcur[ks], S.u.hd.xT[16 * (k >> 2) + drow<R>(k & 3, g)][16 * cg + c], z0[cg]);
+            z0b[cg] = mfma(fcur[ks + 1], S.u.hd.xT[16 * ((k + 1) >> 2) + drow<R>((k + 1) & 3, g)][16 * cg + c],
+                           z0b[cg]);
+          }
+        }
       }
     }
 #pragma unroll
@@ -858,21 +916,19 @@ __device__ void head_stage(const FusedArgs& A, Smem<K, TM, R, NW, DR, NM>& S) {
 #pragma unroll
   for (int t = 1; t < kMaxHidden; ++t) {
     if (t >= A.reg_hidden) break;
-    const R* __restrict__ Af = hid + (t - 1) * HS;
-    const R* __restrict__ ct = Af + 2 * RW * RW;
+    const R* __restrict__ ct = hid + (t - 1) * HS + 2 * RW * RW;
     v4<R> z[CG];
 #pragma unroll
     for (int cg = 0; cg < CG; ++cg) z[cg] = v4<R>{0, 0, 0, 0};
     if (rw) {
+      ADVANCE();
 #pragma unroll
       for (int cg = 0; cg < CG; ++cg) z[cg] = v4<R>{ct[ROW(0)], ct[ROW(1)], ct[ROW(2)], ct[ROW(3)]};
 #pragma unroll
-      for (int ks = 0; ks < 16; ++ks) {
-        const R f = Af[(ks * 4 + w) * 64 + lane];
+      for (int ks = 0; ks < 16; ++ks)
 #pragma unroll
         for (int cg = 0; cg < CG; ++cg)
-          z[cg] = mfma(f, S.u.hd.yT[16 * (ks >> 2) + drow<R>(ks & 3, g)][16 * cg + c], z[cg]);
-      }
+          z[cg] = mfma(fcur[ks], S.u.hd.yT[16 * (ks >> 2) + drow<R>(ks & 3, g)][16 * cg + c], z[cg]);
     }
 #pragma unroll
     for (int cg = 0; cg < CG; ++cg) zeta[t][cg] = z[cg];
@@ -899,7 +955,6 @@ __device__ void head_stage(const FusedArgs& A, Smem<K, TM, R, NW, DR, NM>& S) {
 #pragma unroll
   for (int t = kMaxHidden - 1; t >= 1; --t) {
     if (t >= A.reg_hidden) continue;
-    const R* __restrict__ ATf = hid + (t - 1) * HS + RW * RW;
     if (rw) {
 #pragma unroll
       for (int cg = 0; cg < CG; ++cg)
@@ -911,16 +966,15 @@ __device__ void head_stage(const FusedArgs& A, Smem<K, TM, R, NW, DR, NM>& S) {
     }
     __syncthreads();
     if (rw) {
+      ADVANCE();
       v4<R> acc[CG];
 #pragma unroll
       for (int cg = 0; cg < CG; ++cg) acc[cg] = v4<R>{0, 0, 0, 0};
 #pragma unroll
-      for (int ks = 0; ks < 16; ++ks) {
-        const R f = ATf[(ks * 4 + w) * 64 + lane];
+      for (int ks = 0; ks < 16; ++ks)
 #pragma unroll
         for (int cg = 0; cg < CG; ++cg)
-          acc[cg] = mfma(f, S.u.hd.gT[16 * (ks >> 2) + drow<R>(ks & 3, g)][16 * cg + c], acc[cg]);
-      }
+          acc[cg] = mfma(fcur[ks], S.u.hd.gT[16 * (ks >> 2) + drow<R>(ks & 3, g)][16 * cg + c], acc[cg]);
 #pragma unroll
       for (int cg = 0; cg < CG; ++cg) d[cg] += acc[cg];
     }
@@ -938,15 +992,15 @@ __device__ void head_stage(const FusedArgs& A, Smem<K, TM, R, NW, DR, NM>& S) {
   __syncthreads();
   // dE/dx = A0^T g0, then W[0][col] = dE/dG[0][col], W[m][col] = 2 dE/dG[l][col] P[m][col]
   for (int tt = w; tt < tin; tt += NW) {
+    ADVANCE();
     v4<R> acc[CG];
 #pragma unroll
     for (int cg = 0; cg < CG; ++cg) acc[cg] = v4<R>{0, 0, 0, 0};
 #pragma unroll
     for (int ks = 0; ks < 16; ++ks) {
-      const R f = A0Tf[(ks * tin + tt) * 64 + lane];
 #pragma unroll
       for (int cg = 0; cg < CG; ++cg)
-        acc[cg] = mfma(f, S.u.hd.gT[16 * (ks >> 2) + drow<R>(ks & 3, g)][16 * cg + c], acc[cg]);
+        acc[cg] = mfma(fcur[ks], S.u.hd.gT[16 * (ks >> 2) + drow<R>(ks & 3, g)][16 * cg + c], acc[cg]);
     }
 #pragma unroll
     for (int cg = 0; cg < CG; ++cg) {
@@ -965,6 +1019,7 @@ __device__ void head_stage(const FusedArgs& A, Smem<K, TM, R, NW, DR, NM>& S) {
   }
   __syncthreads();
 #undef ROW
+#undef ADVANCE
 }
 
 // First-layer weights (w0, b0) of the tile's encoder tables, one per
@@ -991,6 +1046,7 @@ static_assert(kRegress == kModeRegress && kRadial == kModeRadial, "mode numbers 
 
 template <int K, int TM, typename R, int NW, int DR, int NM, int MODE>
 __global__ __launch_bounds__(64 * NW, 1) void k_fused(FusedArgs A) {
+  static_assert(TM <= 64, "the bucket table gives one lane to each atom of a tile");
   extern __shared__ __align__(16) unsigned char smem_raw[];
   Smem<K, TM, R, NW, DR, NM>& S = *reinterpret_cast<Smem<K, TM, R, NW, DR, NM>*>(smem_raw);
   const int tid = threadIdx.x, wave = tid >> 6;
@@ -1106,35 +1162,49 @@ __global__ __launch_bounds__(64 * NW, 1) void k_fused(FusedArgs A) {
       prefix = inc - my_active;
       for (int w = 0; w < wave; ++w) prefix += S.wsum[w];
     }
-    if (tid == 0) {
-      // bucket layout: species-major, atoms in order; chunk table; and the
-      // offset turning an entry's block-wide active prefix into its slot
-      int run = 0, nch = 0;
+    if (wave == 0) {
+      // Bucket layout (species-major, atoms in order), chunk table, and the
+      // offset turning an entry's block-wide active prefix (atom-major) into
+      // its bucket slot: base[s][a] = (active entries of buckets before
+      // (s, a) in species-major order) - (active entries before (a, s) in
+      // atom-major order).  Lane a holds atom a; one lane scan per species.
+      const int ln = tid;
+      int run = 0, nchunk = 0, cum = 0;  // cum: this atom's entries of the species so far
       for (int s = 0; s < A.C; ++s) {
-        const int b0 = run;
-        for (int a = 0; a < na; ++a) {
-          S.base[s][a] = run;
-          run += S.cnt[s][a];
+        const int x = ln < na ? S.cnt[s][ln] : 0;
+        int inc = x;
+#pragma unroll
+        for (int o = 1; o < 64; o <<= 1) {
+          const int t = __shfl_up(inc, o, 64);
+          if (ln >= o) inc += t;
         }
-        for (int off = b0; off < run; off += 16) {
-          S.ch_start[nch] = off;
-          S.ch_count[nch] = (unsigned char)(run - off < 16 ? run - off : 16);
-          S.ch_s[nch] = (unsigned char)s;
-          ++nch;
+        const int tot = __shfl(inc, 63, 64);
+        if (ln < na) S.base[s][ln] = run + inc - x - cum;
+        cum += x;
+        const int nb = (tot + 15) >> 4;
+        for (int k = ln; k < nb; k += 64) {
+          S.ch_start[nchunk + k] = run + 16 * k;
+          S.ch_count[nchunk + k] = (unsigned char)(tot - 16 * k < 16 ? tot - 16 * k : 16);
+          S.ch_s[nchunk + k] = (unsigned char)s;
         }
+        nchunk += nb;
+        run += tot;
       }
-      S.n_chunks = nch;
-      S.next_chunk[0] = NW;  // chunk w < NW starts on wavefront w
-      S.next_chunk[1] = NW;
-      S.n_active = run;
-      int row_start = 0;
-      for (int a = 0; a < na; ++a) {
-        int cum = 0;
-        for (int s = 0; s < A.C; ++s) {
-          S.base[s][a] -= row_start + cum;
-          cum += S.cnt[s][a];
-        }
-        row_start += cum;
+      // cum is now this atom's row total; subtract the atom-major row start
+      int inc = cum;
+#pragma unroll
+      for (int o = 1; o < 64; o <<= 1) {
+        const int t = __shfl_up(inc, o, 64);
+        if (ln >= o) inc += t;
+      }
+      const int row_start = inc - cum;
+      if (ln < na)
+        for (int s = 0; s < A.C; ++s) S.base[s][ln] -= row_start;
+      if (ln == 0) {
+        S.n_chunks = nchunk;
+        S.next_chunk[0] = NW;  // chunk w < NW starts on wavefront w
+        S.next_chunk[1] = NW;
+        S.n_active = run;
       }
     }
     __syncthreads();
