@@ -263,7 +263,9 @@ __device__ __forceinline__ PairPos load_pair_pos(const FusedArgs& A, const Smem<
 
 // Weight-fragment streaming of the encoder products: fragments of VW
 // consecutive output tiles per 16-byte load, through register rings issued
-// kRing - 1 k-steps ahead of the MFMAs that consume them.
+// kRing - 1 (hidden layers) or kRingO - 1 (output layer) k-steps ahead of the
+// MFMAs that consume them.  An output-layer k-step is only 2 KT products, so
+// its ring runs further ahead to cover the L2 latency.
 template <int K, typename R>
 struct Stream {
   static constexpr int KT = K / 16;
@@ -272,6 +274,7 @@ struct Stream {
   static constexpr int VO = KT < VW ? KT : VW;    // fragments per output-layer load
   static constexpr int NO = KT / VO;              // loads per output-layer k-step
   static constexpr int kRing = 3;
+  static constexpr int kRingO = 8;
   typedef R vh_t __attribute__((ext_vector_type(VW)));
   typedef R vo_t __attribute__((ext_vector_type(VO)));
 };
@@ -378,7 +381,7 @@ __device__ __forceinline__ void encoder_out_rows(const R* __restrict__ layer, co
                                                  v4<R> (&mo)[K / 16], v4<R> (&dmo)[K / 16]) {
   typedef Stream<K, R> St;
   typedef typename St::vo_t vo_t;
-  constexpr int KT = St::KT, NO = St::NO, VO = St::VO, kRing = St::kRing;
+  constexpr int KT = St::KT, NO = St::NO, VO = St::VO, kRing = St::kRingO;
   const int lane = threadIdx.x & 63, c = lane & 15;
   const R* __restrict__ bout = layer + K * kEncWidth;
   v4<R> mo2[2][KT], dmo2[2][KT];
@@ -428,7 +431,7 @@ __device__ __forceinline__ void encoder_out_cols(const R* __restrict__ layer, co
                                                  R (&mB)[K / 16][4], R (&dmB)[K / 16][4]) {
   typedef Stream<K, R> St;
   typedef typename St::vo_t vo_t;
-  constexpr int KT = St::KT, NO = St::NO, VO = St::VO, kRing = St::kRing;
+  constexpr int KT = St::KT, NO = St::NO, VO = St::VO, kRing = St::kRingO;
   const int lane = threadIdx.x & 63, g = lane >> 4;
   const R* __restrict__ bout = layer + K * kEncWidth;
   v4<R> acc[KT], dacc[KT];
@@ -494,24 +497,27 @@ __device__ void pass1_chunk(const FusedArgs& A, Smem<K, TM, R, NW, DR, NM>& S, i
   // moment: P[mm][col] += sum_pairs fc * a_mm(u) * m[pair][col], one MFMA
   // product per centre atom present in the chunk and 16-row tile of the
   // angular features (pairs of other atoms are masked to zero in the A
-  // operand)
+  // operand).  The features themselves are an MFMA product over the
+  // monomials, F[pair][mm] = sum_m fc m_m(u_pair) Q[mm][m], whose result
+  // registers (register q: pair drow(q, g), row c) are exactly the A operand
+  // of the moment product; each lane forms only its own pair's monomials.
   constexpr int NA = DR / 16;
-  R av[NA][4];
+  static_assert(NM % 4 == 0, "monomial count must be a multiple of the MFMA k-step");
+  v4<R> av[NA];
   int aa[4];
 #pragma unroll
-  for (int q = 0; q < 4; ++q) {
-    const int src = drow<R>(q, g);  // pair index; any lane with c == src holds it
-    const R px = __shfl(ux, src, 64), py = __shfl(uy, src, 64), pz = __shfl(uz, src, 64);
-    const R pf = __shfl(fc, src, 64);
-    aa[q] = __shfl(atom, src, 64);
+  for (int q = 0; q < 4; ++q) aa[q] = __shfl(atom, drow<R>(q, g), 64);
+  {
     R mono[NM];
-    monomials_n<NM, false>(px, py, pz, mono, mono, mono, mono);
+    monomials_n<NM, false>(ux, uy, uz, mono, mono, mono, mono);
 #pragma unroll
-    for (int ta = 0; ta < NA; ++ta) {
-      R s = 0;
+    for (int ta = 0; ta < NA; ++ta) av[ta] = v4<R>{0, 0, 0, 0};
 #pragma unroll
-      for (int m = 0; m < NM; ++m) s += S.qc[16 * ta + c][m] * mono[m];
-      av[ta][q] = pf * s;
+    for (int i = 0; i < NM / 4; ++i) {
+      // A[pair c][m = 4i + g] = fc m_m(u_c); B[m = 4i + g][row c] = Q[row][m]
+      const R x = fc * (g == 0 ? mono[4 * i] : g == 1 ? mono[4 * i + 1] : g == 2 ? mono[4 * i + 2] : mono[4 * i + 3]);
+#pragma unroll
+      for (int ta = 0; ta < NA; ++ta) av[ta] = mfma(x, S.qc[16 * ta + c][4 * i + g], av[ta]);
     }
   }
   const int a_first = S.pair_a[start], a_last = S.pair_a[start + count - 1];
