@@ -142,10 +142,58 @@ __device__ __forceinline__ double vsqrt(double x) { return sqrt(x); }
 __device__ __forceinline__ float vsqrt(float x) { return __builtin_amdgcn_sqrtf(x); }
 __device__ __forceinline__ double vrcp(double x) { return 1.0 / x; }
 __device__ __forceinline__ float vrcp(float x) { return __builtin_amdgcn_rcpf(x); }
-__device__ __forceinline__ double vcos(double x) { return cos(x); }
-__device__ __forceinline__ float vcos(float x) { return __builtin_amdgcn_cosf(x * 0.159154943f); }
-__device__ __forceinline__ double vsin(double x) { return sin(x); }
-__device__ __forceinline__ float vsin(float x) { return __builtin_amdgcn_sinf(x * 0.159154943f); }
+
+// cos(x) and sin(x) for 0 <= x < pi (the cutoff function's argument, x =
+// pi r / r_c with r < r_c) in float64: Cody-Waite reduction x = k pi/2 + y
+// with k = rint(2x / pi) in {0, 1, 2} and |y| <= pi/4, the Taylor
+// polynomials of sin (degree 13) and cos (degree 14) in y (truncation below
+// 2e-14 and 1e-15 relative), then the quadrant rotation.  The general library
+// routines carry range reduction for any argument, which this path never
+// needs.
+__device__ __forceinline__ void cut_sincos(double x, double* sn, double* cs) {
+  constexpr double kTwoOverPi = 0.63661977236758134308;
+  constexpr double kPio2Hi = 1.57079632679489655800e+00;  // pi/2 = hi + lo
+  constexpr double kPio2Lo = 6.12323399573676603587e-17;
+  const double k = rint(x * kTwoOverPi);
+  double y = fma(-k, kPio2Hi, x);
+  y = fma(-k, kPio2Lo, y);
+  const double y2 = y * y;
+  // 1 / n! for the odd (sin) and even (cos) terms, highest first
+  double ps = 1.6059043836821613e-10;   // 1/13!
+  ps = fma(ps, y2, -2.505210838544172e-08);  // -1/11!
+  ps = fma(ps, y2, 2.7557319223985893e-06);  // 1/9!
+  ps = fma(ps, y2, -1.984126984126984e-04);  // -1/7!
+  ps = fma(ps, y2, 8.333333333333333e-03);   // 1/5!
+  ps = fma(ps, y2, -1.6666666666666666e-01); // -1/3!
+  const double sy = fma(ps * y2, y, y);
+  double pc = -1.1470745597729725e-11;  // -1/14!
+  pc = fma(pc, y2, 2.08767569878681e-09);    // 1/12!
+  pc = fma(pc, y2, -2.755731922398589e-07);  // -1/10!
+  pc = fma(pc, y2, 2.48015873015873e-05);    // 1/8!
+  pc = fma(pc, y2, -1.388888888888889e-03);  // -1/6!
+  pc = fma(pc, y2, 4.1666666666666664e-02);  // 1/4!
+  pc = fma(pc, y2, -0.5);                    // -1/2!
+  const double cy = fma(pc, y2, 1.0);
+  const int q = int(k);
+  *sn = q == 0 ? sy : (q == 1 ? cy : -sy);
+  *cs = q == 0 ? cy : (q == 1 ? -sy : -cy);
+}
+
+// Cutoff function fc(r) = (1 + cos(pi r / r_c)) / 2 and its derivative
+// -(pi / r_c) sin(pi r / r_c) / 2 for r < r_c (Eq. 2): float64 from the
+// reduced-range routine above, float32 from the hardware sine and cosine
+// (about one ulp; they take revolutions).
+__device__ __forceinline__ void cutoff(double r, double pi_rc, double* fc, double* dfc) {
+  double sn, cs;
+  cut_sincos(r * pi_rc, &sn, &cs);
+  *fc = 0.5 * (1.0 + cs);
+  *dfc = -0.5 * pi_rc * sn;
+}
+__device__ __forceinline__ void cutoff(float r, float pi_rc, float* fc, float* dfc) {
+  const float x = r * pi_rc * 0.159154943f;
+  *fc = 0.5f * (1.0f + __builtin_amdgcn_cosf(x));
+  *dfc = -0.5f * pi_rc * __builtin_amdgcn_sinf(x);
+}
 
 // Exponents (a, b, c) of the Cartesian monomials of degree <= 5, degree by
 // degree and lexicographic with x first within a degree (the column order of
@@ -375,7 +423,8 @@ __device__ __forceinline__ const R* encoder_hidden(const FusedArgs& A, const Sme
 // Encoder output layer with pairs as rows: mo[Tc] register q holds
 // m[pair drow(q, g)][16Tc + c] (dmo the same for the tangent).  Even and odd
 // k-steps accumulate separately so 4 KT independent MFMA chains are in
-// flight.
+// flight; the bias is added at the end so the first products do not wait
+// for its load.
 template <int K, typename R>
 __device__ __forceinline__ void encoder_out_rows(const R* __restrict__ layer, const R (&h)[8][4], const R (&dh)[8][4],
                                                  v4<R> (&mo)[K / 16], v4<R> (&dmo)[K / 16]) {
@@ -385,13 +434,11 @@ __device__ __forceinline__ void encoder_out_rows(const R* __restrict__ layer, co
   const int lane = threadIdx.x & 63, c = lane & 15;
   const R* __restrict__ bout = layer + K * kEncWidth;
   v4<R> mo2[2][KT], dmo2[2][KT];
+  R b[KT];
 #pragma unroll
   for (int Tc = 0; Tc < KT; ++Tc) {
-    const R b = bout[16 * Tc + c];
-    mo2[0][Tc] = v4<R>{b, b, b, b};
-    mo2[1][Tc] = v4<R>{0, 0, 0, 0};
-    dmo2[0][Tc] = v4<R>{0, 0, 0, 0};
-    dmo2[1][Tc] = v4<R>{0, 0, 0, 0};
+    b[Tc] = bout[16 * Tc + c];
+    mo2[0][Tc] = mo2[1][Tc] = dmo2[0][Tc] = dmo2[1][Tc] = v4<R>{0, 0, 0, 0};
   }
   const vo_t* __restrict__ frag = reinterpret_cast<const vo_t*>(layer) + lane;
   vo_t wo[kRing][NO];
@@ -417,7 +464,7 @@ __device__ __forceinline__ void encoder_out_rows(const R* __restrict__ layer, co
   }
 #pragma unroll
   for (int Tc = 0; Tc < KT; ++Tc) {
-    mo[Tc] = mo2[0][Tc] + mo2[1][Tc];
+    mo[Tc] = mo2[0][Tc] + mo2[1][Tc] + v4<R>{b[Tc], b[Tc], b[Tc], b[Tc]};
     dmo[Tc] = dmo2[0][Tc] + dmo2[1][Tc];
   }
 }
@@ -478,7 +525,9 @@ template <int K, int TM, typename R, int NW, int DR, int NM, bool kWs>
 __device__ void pass1_chunk(const FusedArgs& A, Smem<K, TM, R, NW, DR, NM>& S, int ch, const PairPos pp, R* __restrict__ wsc) {
   constexpr int KT = K / 16;
   const int lane = threadIdx.x & 63, g = lane >> 4, c = lane & 15;
-  const int start = S.ch_start[ch], count = S.ch_count[ch];
+  // chunk-wide values, in scalar registers
+  const int start = __builtin_amdgcn_readfirstlane(S.ch_start[ch]);
+  const int count = __builtin_amdgcn_readfirstlane(S.ch_count[ch]);
 
   double dxd, dyd, dzd;
   int atom;
@@ -487,7 +536,9 @@ __device__ void pass1_chunk(const FusedArgs& A, Smem<K, TM, R, NW, DR, NM>& S, i
   const R r = vsqrt(dx * dx + dy * dy + dz * dz);
   const R ir = vrcp(r);
   const R ux = dx * ir, uy = dy * ir, uz = dz * ir;
-  const R fc = atom >= 0 ? R(0.5) * (R(1) + vcos(r * R(A.pi_rc))) : R(0);
+  R fc, dfc_unused;
+  cutoff(r, R(A.pi_rc), &fc, &dfc_unused);
+  if (atom < 0) fc = R(0);
 
   R h[8][4], dh[8][4];
   const R* __restrict__ layer = encoder_hidden(A, S, S.ch_s[ch], r, chunk_table(A, S, ch), h, dh);
@@ -520,7 +571,8 @@ __device__ void pass1_chunk(const FusedArgs& A, Smem<K, TM, R, NW, DR, NM>& S, i
       for (int ta = 0; ta < NA; ++ta) av[ta] = mfma(x, S.qc[16 * ta + c][4 * i + g], av[ta]);
     }
   }
-  const int a_first = S.pair_a[start], a_last = S.pair_a[start + count - 1];
+  const int a_first = __builtin_amdgcn_readfirstlane(S.pair_a[start]);
+  const int a_last = __builtin_amdgcn_readfirstlane(S.pair_a[start + count - 1]);
   for (int a = a_first; a <= a_last; ++a) {
 #pragma unroll
     for (int ta = 0; ta < NA; ++ta) {
@@ -609,7 +661,9 @@ template <int K, int TM, typename R, int NW, int DR, int NM>
 __device__ void pass2_chunk(const FusedArgs& A, Smem<K, TM, R, NW, DR, NM>& S, int ch, const Pass2In<K, R>& in) {
   constexpr int KT = K / 16;
   const int lane = threadIdx.x & 63, g = lane >> 4, c = lane & 15;
-  const int start = S.ch_start[ch], count = S.ch_count[ch];
+  // chunk-wide values, in scalar registers
+  const int start = __builtin_amdgcn_readfirstlane(S.ch_start[ch]);
+  const int count = __builtin_amdgcn_readfirstlane(S.ch_count[ch]);
 
   const bool valid = c < count;
   int atom = -1, j = 0;
@@ -626,9 +680,9 @@ __device__ void pass2_chunk(const FusedArgs& A, Smem<K, TM, R, NW, DR, NM>& S, i
   const R r = vsqrt(rx * rx + ry * ry + rz * rz);
   const R ir = vrcp(r);
   const R ux = rx * ir, uy = ry * ir, uz = rz * ir;
-  const R arg = r * R(A.pi_rc);
-  const R fc = valid ? R(0.5) * (R(1) + vcos(arg)) : R(0);
-  const R dfc = valid ? R(-0.5) * R(A.pi_rc) * vsin(arg) : R(0);
+  R fc, dfc;
+  cutoff(r, R(A.pi_rc), &fc, &dfc);
+  if (!valid) fc = dfc = R(0);
 
   // (W m) and (W dm) for this column's own centre atom, one 16-row tile of
   // the angular features at a time
@@ -636,7 +690,8 @@ __device__ void pass2_chunk(const FusedArgs& A, Smem<K, TM, R, NW, DR, NM>& S, i
   v4<R> wm[NA], wdm[NA];
 #pragma unroll
   for (int ta = 0; ta < NA; ++ta) wm[ta] = wdm[ta] = v4<R>{0, 0, 0, 0};
-  const int a_first = S.pair_a[start], a_last = S.pair_a[start + count - 1];
+  const int a_first = __builtin_amdgcn_readfirstlane(S.pair_a[start]);
+  const int a_last = __builtin_amdgcn_readfirstlane(S.pair_a[start + count - 1]);
   for (int a = a_first; a <= a_last; ++a) {
 #pragma unroll
     for (int ta = 0; ta < NA; ++ta) {
@@ -738,9 +793,9 @@ __device__ void radial_chunk(const FusedArgs& A, const Smem<K, TM, R, NW, DR, NM
   const bool valid = c < S.ch_count[ch];
   const long long e = S.row_beg[0] + (valid ? S.pair_j[S.ch_start[ch] + c] : 0);
   const R r = valid ? R(A.geo[4 * e + 3]) : R(1);
-  const R arg = r * R(A.pi_rc);
-  const R fc = valid ? R(0.5) * (R(1) + vcos(arg)) : R(0);
-  const R dfc = valid ? R(-0.5) * R(A.pi_rc) * vsin(arg) : R(0);
+  R fc, dfc;
+  cutoff(r, R(A.pi_rc), &fc, &dfc);
+  if (!valid) fc = dfc = R(0);
   R h[8][4], dh[8][4];
   const R* __restrict__ layer = encoder_hidden(A, S, S.ch_s[ch], r, chunk_table(A, S, ch), h, dh);
   R mB[KT][4], dmB[KT][4];
