@@ -129,10 +129,21 @@ __global__ void k_rows(const double* __restrict__ spos, const int32_t* __restric
   const int64_t base = kFill ? offsets[a] : 0;
   for (int s = 0; s < g.C; ++s) {
     for (int iz = 0; iz < nz; ++iz)
-      for (int iy = 0; iy < ny; ++iy)
-        for (int ix = 0; ix < nx; ++ix) {
-          const int key = s * g.ncell + (zs[iz] * g.nc[1] + ys[iy]) * g.nc[0] + xs[ix];
-          const int e = start[key + 1];
+      for (int iy = 0; iy < ny; ++iy) {
+        // x-neighbour cells with consecutive indices are consecutive keys, so
+        // their atoms form one run of the sorted order: visit runs, not cells
+        // (same entries in the same order)
+        int ix = 0;
+        while (ix < nx) {
+          const int x0 = xs[ix];
+          int x1 = x0;
+          while (ix + 1 < nx && xs[ix + 1] == x1 + 1) {
+            ++ix;
+            ++x1;
+          }
+          ++ix;
+          const int key = s * g.ncell + (zs[iz] * g.nc[1] + ys[iy]) * g.nc[0] + x0;
+          const int e = start[key + (x1 - x0) + 1];
           for (int b = start[key]; b < e; ++b) {
             if (b == a) continue;
             const double dx = fold(spos[3 * int64_t(b)] - wx, g.box[0], g.half[0]);
@@ -144,6 +155,7 @@ __global__ void k_rows(const double* __restrict__ spos, const int32_t* __restric
             }
           }
         }
+      }
   }
   if (!kFill) {
     rowcnt[a] = cnt;
