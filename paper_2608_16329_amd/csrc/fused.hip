@@ -313,7 +313,9 @@ __device__ __forceinline__ PairPos load_pair_pos(const FusedArgs& A, const Smem<
 // consecutive output tiles per 16-byte load, through register rings issued
 // kRing - 1 (hidden layers) or kRingO - 1 (output layer) k-steps ahead of the
 // MFMAs that consume them.  An output-layer k-step is only 2 KT products, so
-// its ring runs further ahead to cover the L2 latency.
+// its ring runs further ahead.  The float32 kernel runs two wavefronts per
+// SIMD, which cover each other's load latency; there shallower rings leave
+// more registers and measured faster (ring depths 2 and 4 against 3 and 8).
 template <int K, typename R>
 struct Stream {
   static constexpr int KT = K / 16;
@@ -321,8 +323,8 @@ struct Stream {
   static constexpr int NH = 8 / VW;               // loads per hidden-layer k-step
   static constexpr int VO = KT < VW ? KT : VW;    // fragments per output-layer load
   static constexpr int NO = KT / VO;              // loads per output-layer k-step
-  static constexpr int kRing = 3;
-  static constexpr int kRingO = 8;
+  static constexpr int kRing = sizeof(R) == 8 ? 3 : 2;
+  static constexpr int kRingO = sizeof(R) == 8 ? 8 : 4;
   typedef R vh_t __attribute__((ext_vector_type(VW)));
   typedef R vo_t __attribute__((ext_vector_type(VO)));
 };
