@@ -414,6 +414,7 @@ def main() -> int:
     wall = time.perf_counter() - t0
     kern = [a.elapsed_time(b) for a, b in compute_ms]
     ms_compute = float(np.mean(kern))
+    ms_median = float(np.median(kern))
     flop = float(np.mean(active_pairs)) * flops_per_pair(w.hp) + N * flops_per_atom(w.hp)
     achieved = flop / (ms_compute * 1e-3) / 1e12
     value = N * args.steps / wall
@@ -423,6 +424,7 @@ def main() -> int:
     used = free0 - free1
     bpa = used / N
 
+    traffic = measured_traffic(w.description, N, args.precision) if args.fusion == "cached" else None
     result = {
         "metric": "atom-steps/s (E+F+virial) at 1 GPU",
         "value": value,
@@ -446,7 +448,8 @@ def main() -> int:
                    "reg_hidden": w.hp.reg_hidden, "fusion": args.fusion},
         "roofline": {"bound": "mfma", "achieved": achieved, "peak": PEAK_TFLOPS[args.precision], "unit": "TFLOP/s",
                      "frac": achieved / PEAK_TFLOPS[args.precision],
-                     "traffic": measured_traffic(w.description, N, args.precision) if args.fusion == "cached" else None,
+                     "traffic": traffic,
+                     "traffic_gbps": traffic / (ms_compute * 1e-3) / 1e9 if traffic else None,
                      "kernel": {"cached": "fused energy/force/virial (k_fused)",
                                 "recompute": "fused energy/force/virial (k_fused)",
                                 "partial": "encoding + regression + derivation kernels (k_fused modes 2-4)",
@@ -454,6 +457,7 @@ def main() -> int:
                                            "descriptor, regression, adjoint, U, V, force)"}[args.fusion],
                      "kernel_ms": ms_compute,
                      "algorithmic_flop_per_launch": flop},
+        "compute_only_atom_evals_per_s": N / (ms_median * 1e-3),
         "hbm_bytes_per_atom": bpa,
         "library_bytes_per_atom": lib_bytes / N,
         "caller_bytes_per_atom": caller_bytes / N,
