@@ -90,9 +90,10 @@ __device__ __forceinline__ int gof(int c) {
 // matrix products):
 //  * exp(t), t = -z clamped to [-700, 700] (beyond that the sigmoid is 0 or 1
 //    to far below float64 resolution of the SiLU value), by Cody-Waite
-//    reduction t = n ln2 + r with |r| <= ln2/2, the Taylor polynomial of
-//    degree 11 (truncation error (ln2/2)^12 / 12! < 7e-15 relative) and a
-//    2^n scaling;
+//    reduction t = n ln2 + r with |r| <= ln2/2, a degree-10 polynomial (the
+//    interpolant at Chebyshev nodes, below 3.4e-16 relative error; one
+//    degree less, 1.9e-14, let deep networks drift to 6e-10 of the float64
+//    oracle) and a 2^n scaling;
 //  * 1 / (1 + e) from the hardware reciprocal estimate (relative error below
 //    2^-22) refined by one Newton-Raphson step, which squares that error.
 __device__ __forceinline__ double sigmoid(double z) {
@@ -103,23 +104,16 @@ __device__ __forceinline__ double sigmoid(double z) {
   const double n = rint(t * kLog2e);
   double r = fma(-n, kLn2Hi, t);
   r = fma(-n, kLn2Lo, r);
-  // 1 / k! for k = 11 .. 0
-  constexpr double c[12] = {
-    2.505210838544172e-08,
-    2.755731922398589e-07,
-    2.7557319223985893e-06,
-    2.48015873015873e-05,
-    0.0001984126984126984,
-    0.001388888888888889,
-    0.008333333333333333,
-    0.041666666666666664,
-    0.16666666666666666,
-    0.5,
-    1.0,
-    1.0};
+  // polynomial interpolating exp at the 11 Chebyshev nodes of [-ln2/2,
+  // ln2/2] (solved in 80-bit arithmetic, rounded to float64), highest power
+  // first; relative error below 3.4e-16 on the interval
+  constexpr double c[11] = {
+    2.762635356445665e-07,  2.764018186396873e-06, 2.4801504368699663e-05, 0.00019841170267682938,
+    0.0013888888932453442,  0.008333333385670185,  0.04166666666657336,    0.16666666666554397,
+    0.5000000000000006,     1.0000000000000067,    1.0};
   double p = c[0];
 #pragma unroll
-  for (int k = 1; k < 12; ++k) p = fma(p, r, c[k]);
+  for (int k = 1; k < 11; ++k) p = fma(p, r, c[k]);
   const double d = 1.0 + ldexp(p, int(n));
   const double y = __builtin_amdgcn_rcp(d);
   return fma(fma(-d, y, 1.0), y, y);
@@ -146,8 +140,9 @@ __device__ __forceinline__ float vrcp(float x) { return __builtin_amdgcn_rcpf(x)
 // cos(x) and sin(x) for 0 <= x < pi (the cutoff function's argument, x =
 // pi r / r_c with r < r_c) in float64: Cody-Waite reduction x = k pi/2 + y
 // with k = rint(2x / pi) in {0, 1, 2} and |y| <= pi/4, the Taylor
-// polynomials of sin (degree 13) and cos (degree 14) in y (truncation below
-// 2e-14 and 1e-15 relative), then the quadrant rotation.  The general library
+// polynomials of sin (degree 15) and cos (degree 16) in y (truncation below
+// 5e-17 and 3e-18; at degrees 13 and 14 the 2e-14 error of fc reached 6e-10
+// in the forces of deep networks), then the quadrant rotation.  The general library
 // routines carry range reduction for any argument, which this path never
 // needs.
 __device__ __forceinline__ void cut_sincos(double x, double* sn, double* cs) {
@@ -159,14 +154,16 @@ __device__ __forceinline__ void cut_sincos(double x, double* sn, double* cs) {
   y = fma(-k, kPio2Lo, y);
   const double y2 = y * y;
   // 1 / n! for the odd (sin) and even (cos) terms, highest first
-  double ps = 1.6059043836821613e-10;   // 1/13!
+  double ps = -7.647163731819816e-13;  // -1/15!
+  ps = fma(ps, y2, 1.6059043836821613e-10);  // 1/13!
   ps = fma(ps, y2, -2.505210838544172e-08);  // -1/11!
   ps = fma(ps, y2, 2.7557319223985893e-06);  // 1/9!
   ps = fma(ps, y2, -1.984126984126984e-04);  // -1/7!
   ps = fma(ps, y2, 8.333333333333333e-03);   // 1/5!
   ps = fma(ps, y2, -1.6666666666666666e-01); // -1/3!
   const double sy = fma(ps * y2, y, y);
-  double pc = -1.1470745597729725e-11;  // -1/14!
+  double pc = 4.779477332387385e-14;  // 1/16!
+  pc = fma(pc, y2, -1.1470745597729725e-11); // -1/14!
   pc = fma(pc, y2, 2.08767569878681e-09);    // 1/12!
   pc = fma(pc, y2, -2.755731922398589e-07);  // -1/10!
   pc = fma(pc, y2, 2.48015873015873e-05);    // 1/8!
