@@ -91,11 +91,11 @@ __device__ __forceinline__ int gof(int c) {
 //  * exp(t), t = -z clamped to [-700, 700] (beyond that the sigmoid is 0 or 1
 //    to far below float64 resolution of the SiLU value), by Cody-Waite
 //    reduction t = n ln2 + r with |r| <= ln2/2, a degree-10 polynomial (the
-//    interpolant at Chebyshev nodes, below 3.4e-16 relative error; one
-//    degree less, 1.9e-14, let deep networks drift to 6e-10 of the float64
-//    oracle) and a 2^n scaling;
-//  * 1 / (1 + e) from the hardware reciprocal estimate (relative error below
-//    2^-22) refined by one Newton-Raphson step, which squares that error.
+//    interpolant at Chebyshev nodes, below 3.4e-16 relative error) and a 2^n
+//    scaling;
+//  * 1 / (1 + e) from the hardware reciprocal estimate (relative error
+//    measured below 2^-24) refined by one Newton-Raphson step, which squares
+//    that error.
 __device__ __forceinline__ double sigmoid(double z) {
   constexpr double kLog2e = 1.4426950408889634;
   constexpr double kLn2Hi = 6.93147180369123816490e-01;  // ln2 split, high part exact in 32 bits
@@ -130,8 +130,8 @@ __device__ __forceinline__ float sigmoid(float z) {
 }
 
 // Pair geometry after the minimum-image difference (which stays in float64):
-// IEEE float64 operations, or the float32 hardware instructions (about one
-// ulp; sine and cosine take revolutions, valid here since 0 <= x <= pi).
+// IEEE float64 square root and division, or the float32 hardware
+// instructions (about one ulp).
 __device__ __forceinline__ double vsqrt(double x) { return sqrt(x); }
 __device__ __forceinline__ float vsqrt(float x) { return __builtin_amdgcn_sqrtf(x); }
 __device__ __forceinline__ double vrcp(double x) { return 1.0 / x; }
@@ -142,9 +142,9 @@ __device__ __forceinline__ float vrcp(float x) { return __builtin_amdgcn_rcpf(x)
 // with k = rint(2x / pi) in {0, 1, 2} and |y| <= pi/4, the Taylor
 // polynomials of sin (degree 15) and cos (degree 16) in y (truncation below
 // 5e-17 and 3e-18; at degrees 13 and 14 the 2e-14 error of fc reached 6e-10
-// in the forces of deep networks), then the quadrant rotation.  The general library
-// routines carry range reduction for any argument, which this path never
-// needs.
+// in the forces of deep networks), then the quadrant rotation.  The general
+// library routines carry range reduction for any argument, which this path
+// never needs.
 __device__ __forceinline__ void cut_sincos(double x, double* sn, double* cs) {
   constexpr double kTwoOverPi = 0.63661977236758134308;
   constexpr double kPio2Hi = 1.57079632679489655800e+00;  // pi/2 = hi + lo
@@ -194,7 +194,7 @@ __device__ __forceinline__ void cutoff(float r, float pi_rc, float* fc, float* d
 
 // Exponents (a, b, c) of the Cartesian monomials of degree <= 5, degree by
 // degree and lexicographic with x first within a degree (the column order of
-// the angular table; its first 20 entries are the order above).
+// the angular table; its first 20 entries are the order of `monomials`).
 struct MonoExp {
   unsigned char e[56][3];
   constexpr MonoExp() : e{} {
