@@ -283,9 +283,22 @@ def cpu_baseline(w, target_atoms: int) -> dict:
         pool.map(_oracle_worker, jobs)
     wall = time.perf_counter() - t0
     return {"value": len(centres) / wall, "unit": "atom-steps/s", "cores": len(jobs), "kind": "oracle",
+            "cpu_model": host_cpu_model(),
             "sample": f"{len(centres)} centre atoms of the same workload (a cube at the box centre), "
                       f"one E+F+virial evaluation each, float64 NumPy, {len(jobs)} processes x 1 BLAS "
                       f"thread, {wall:.1f} s wall; neighbour search not timed"}
+
+
+def host_cpu_model() -> str:
+    """The host CPU's model name (first processor in /proc/cpuinfo)."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
 
 
 def main() -> int:
