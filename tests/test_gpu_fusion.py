@@ -140,3 +140,25 @@ def test_fusion_argument_checks():
             pot.set_fusion(fusion)
     pot.set_fusion(0)
     pot.close()
+
+
+@pytest.mark.parametrize("precision", [64, 32])
+def test_configurations_agree_at_scale(precision):
+    """At 16,000 atoms of the six-component BCC alloy (hundreds of tiles and
+    work-groups, long unfused grids) every configuration matches the default
+    cached one, which the other tests pin to the oracle, on all atoms."""
+    w = synth.make_workload("bcc-hea6-sweep", seed=17, n=20, hp_overrides={"precision": precision})
+    out = {f: _eval(w.hp, w, f) for f in (0, 1, 2, 3)}
+    for f in (1, 2, 3):
+        for key in ("E_i", "F", "virial"):
+            if precision == 64:
+                d = max_abs(out[f][key], out[0][key])
+                log(f"[fusion] N={len(w.pos)} fp64 {f} vs cached {key}: {d:.2e}")
+                assert d <= TOL64
+            else:
+                d = _rel(out[f][key], out[0][key])
+                log(f"[fusion] N={len(w.pos)} fp32 {f} vs cached {key}: rel {d:.2e}")
+                assert d <= REL32
+        assert out[f]["stats"]["n_active_pairs"] == out[0]["stats"]["n_active_pairs"]
+    for g in out.values():
+        g["pot"].close()
