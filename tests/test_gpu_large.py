@@ -149,3 +149,39 @@ def test_bcc_six_component_sweep_shape_sampled():
     log(f"[large] bcc sweep shape: max|dE|={eE:.2e} max|dF|={eF:.2e} max|dW|={eV:.2e}")
     assert max(eE, eF, eV) <= 1e-9
     pot.close()
+
+
+def test_fusion_configurations_full_size():
+    """On the 8.4M-atom six-component FCC workload the recompute and
+    three-kernel configurations match the cached one (pinned to the oracle
+    above) on every atom; the unfused one does not fit and reports OOM."""
+    import torch
+    from paper_2608_16329_amd import Potential, MlipError
+    w = synth.make_workload("fcc-hea6-128", seed=0)
+    N = len(w.pos)
+    dev = torch.device("cuda:0")
+    pot = Potential(w.hp, w.weights)
+    pos = to_dev(w.pos)
+    types = to_dev(w.types)
+    pot.build_neighbors(pos, types, w.box)
+    res = {}
+    for fusion in (0, 1, 2):
+        pot.set_fusion(fusion)
+        F = torch.empty((N, 3), dtype=torch.float64, device=dev)
+        E = torch.empty(N, dtype=torch.float64, device=dev)
+        V = torch.empty((N, 9), dtype=torch.float64, device=dev)
+        log(f"[large] fusion {fusion}: compute")
+        pot.compute(pos, F, E, V)
+        torch.cuda.synchronize()
+        res[fusion] = (E, F, V)
+    for fusion in (1, 2):
+        d = [(res[fusion][k] - res[0][k]).abs().max().item() for k in range(3)]
+        log(f"[large] fusion {fusion} vs cached on {N} atoms: max|dE|={d[0]:.2e} max|dF|={d[1]:.2e} max|dW|={d[2]:.2e}")
+        assert max(d) <= TOL
+    del res
+    torch.cuda.empty_cache()
+    pot.set_fusion(3)
+    F = torch.empty((N, 3), dtype=torch.float64, device=dev)
+    with pytest.raises(MlipError, match="OOM"):
+        pot.compute(pos, F)
+    pot.close()
