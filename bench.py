@@ -7,7 +7,9 @@ and the second half kick.  Inputs are resident in HBM before timing starts.
 
 Default workload: 6-component equiatomic random FCC alloy, 128^3 cells =
 8,388,608 atoms, a = 3.6 A, sigma = 0.1 A, cutoff 6.0 A, skin 0.5 A, k = 32,
-l_max = 3, encoder 3 x 128, head 4 x 64, random N(0, 1/fan_in) weights.
+l_max = 3, encoder 3 x 128, head 4 x 64, random N(0, 1/fan_in) weights with the
+head's output layer scaled so forces are about 1 eV/A, as from a trained
+potential near 300 K (the values change no work).
 
 Prints one JSON line (rank 0, one GPU).
 """
@@ -162,7 +164,7 @@ def capacity_sweep(edges, steps: int, seed: int, bpa: float = 450.0, precision: 
             print(json.dumps({"sweep_edge": L, "n_atoms": N, "fits": False}), flush=True)
             continue
         hp = synth.HParams(n_species=p["C"], cutoff=p["cutoff"], skin=0.5, precision=precision)
-        weights = synth.random_weights(hp, seed + 1)
+        weights = synth.random_weights(hp, seed + 1, energy_scale=synth.PHYSICAL_ENERGY_SCALE)
         masses = np.array([synth.MASS[x] for x in p["masses"]])
         box = np.array([L * p["a"]] * 3)
         t0 = time.perf_counter()
@@ -352,7 +354,8 @@ def main() -> int:
     for item in filter(None, args.hp.split(",")):
         key, val = item.split("=")
         overrides[key.strip()] = int(val)
-    w = synth.make_workload(args.workload, seed=args.seed, n=args.cells, hp_overrides=overrides)
+    w = synth.make_workload(args.workload, seed=args.seed, n=args.cells, hp_overrides=overrides,
+                            energy_scale=synth.PHYSICAL_ENERGY_SCALE)
     N = len(w.pos)
     log(f"[bench] workload {w.description}: N={N} generated in {time.perf_counter() - t_gen:.1f}s")
     dev = torch.device("cuda:0")
@@ -454,6 +457,7 @@ def main() -> int:
         "config": {"workload": w.description, "n_atoms": N, "n_species": w.hp.n_species, "k": w.hp.k,
                    "lmax": w.hp.lmax, "cutoff": w.hp.cutoff, "skin": w.hp.skin, "dt_fs": dt,
                    "rebuild_every": args.rebuild_every, "rebuilds_in_timed_steps": rebuilds,
+                   "head_output_scale": synth.PHYSICAL_ENERGY_SCALE,
                    "active_pairs_per_atom": float(np.mean(active_pairs)) / N,
                    "listed_pairs_per_atom": st["n_listed_pairs"] / N, "tile_atoms": st["tile_atoms"],
                    "blocks": st["n_blocks"], "seed": args.seed, "precision": args.precision,

@@ -284,6 +284,21 @@ struct PairPos {
   double x, y, z;
 };
 
+// Value of group g (0..3) among four, by bit masks: a select chain on the
+// lane-dependent g would otherwise be compiled into divergent branches.
+__device__ __forceinline__ double pick4(int g, double m0, double m1, double m2, double m3) {
+  const unsigned long long s1 = 0ull - (unsigned long long)(g & 1), s2 = 0ull - (unsigned long long)((g >> 1) & 1);
+  const unsigned long long lo = (__double_as_longlong(m0) & ~s1) | (__double_as_longlong(m1) & s1);
+  const unsigned long long hi = (__double_as_longlong(m2) & ~s1) | (__double_as_longlong(m3) & s1);
+  return __longlong_as_double((long long)((lo & ~s2) | (hi & s2)));
+}
+__device__ __forceinline__ float pick4(int g, float m0, float m1, float m2, float m3) {
+  const unsigned s1 = 0u - unsigned(g & 1), s2 = 0u - unsigned((g >> 1) & 1);
+  const unsigned lo = (__float_as_uint(m0) & ~s1) | (__float_as_uint(m1) & s1);
+  const unsigned hi = (__float_as_uint(m2) & ~s1) | (__float_as_uint(m3) & s1);
+  return __uint_as_float((lo & ~s2) | (hi & s2));
+}
+
 // Next chunk for this wavefront: chunks are handed out in order from an LDS
 // counter, so a wavefront that runs ahead of its SIMD partner takes more of
 // them and the wavefronts of a tile finish together.
@@ -565,7 +580,7 @@ __device__ void pass1_chunk(const FusedArgs& A, Smem<K, TM, R, NW, DR, NM>& S, i
 #pragma unroll
     for (int i = 0; i < NM / 4; ++i) {
       // A[pair c][m = 4i + g] = fc m_m(u_c); B[m = 4i + g][row c] = Q[row][m]
-      const R x = fc * (g == 0 ? mono[4 * i] : g == 1 ? mono[4 * i + 1] : g == 2 ? mono[4 * i + 2] : mono[4 * i + 3]);
+      const R x = fc * pick4(g, mono[4 * i], mono[4 * i + 1], mono[4 * i + 2], mono[4 * i + 3]);
 #pragma unroll
       for (int ta = 0; ta < NA; ++ta) av[ta] = mfma(x, S.qc[16 * ta + c][4 * i + g], av[ta]);
     }

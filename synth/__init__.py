@@ -96,10 +96,27 @@ def weight_count(hp: HParams) -> int:
     return sum(n for _, n, _ in weight_segments(hp))
 
 
-def random_weights(hp: HParams, seed: int, scale: float = 1.0) -> np.ndarray:
-    """Weights and biases drawn N(0, scale^2/fan_in), segment by segment."""
+# Factor on the energy head's output layer for workloads that run MD.  With
+# every layer drawn N(0, 1/fan_in) the descriptor is unnormalised and a
+# thermalised alloy sees forces of about 100 eV/A, which carry atoms past half
+# the neighbour-list skin within a few 1 fs steps and melt the lattice.  Scaled
+# by this factor the mean force is about 1 eV/A, the size a trained potential
+# gives near 300 K, so the list lasts its 10 steps as in production runs.  The
+# values change no work: every pair and atom is evaluated the same way.
+PHYSICAL_ENERGY_SCALE = 0.01
+
+
+def random_weights(hp: HParams, seed: int, scale: float = 1.0, energy_scale: float = 1.0) -> np.ndarray:
+    """Weights and biases drawn N(0, scale^2/fan_in), segment by segment; the
+    head's output layer (weights and bias) is then multiplied by energy_scale,
+    which scales energies, forces and virials by the same factor."""
     rng = np.random.default_rng(seed)
-    parts = [rng.normal(0.0, scale / math.sqrt(fan), n) for _, n, fan in weight_segments(hp)]
+    segs = weight_segments(hp)
+    parts = [rng.normal(0.0, scale / math.sqrt(fan), n) for _, n, fan in segs]
+    if energy_scale != 1.0:
+        for i, (name, _, _) in enumerate(segs):
+            if name.endswith(".aout") or name.endswith(".cout"):
+                parts[i] = parts[i] * energy_scale
     return np.concatenate(parts).astype(np.float64)
 
 
@@ -188,7 +205,8 @@ PRESETS: Dict[str, dict] = {
 
 
 def make_workload(name: str, seed: int = 0, n: Optional[int] = None, skin: float = 0.5,
-                  hp_overrides: Optional[dict] = None, weight_scale: float = 1.0) -> Workload:
+                  hp_overrides: Optional[dict] = None, weight_scale: float = 1.0,
+                  energy_scale: float = 1.0) -> Workload:
     """Build a named workload.  `n` overrides the supercell edge (in cells)."""
     p = PRESETS[name]
     rng = np.random.default_rng(seed)
@@ -206,7 +224,7 @@ def make_workload(name: str, seed: int = 0, n: Optional[int] = None, skin: float
     hp = HParams(n_species=C, cutoff=p["cutoff"], skin=skin)
     for key, val in (hp_overrides or {}).items():
         setattr(hp, key, val)
-    weights = random_weights(hp, seed + 1, weight_scale)
+    weights = random_weights(hp, seed + 1, weight_scale, energy_scale)
     return Workload(name=name, pos=pos, types=types, box=box, vel=vel, masses=masses, hp=hp,
                     weights=weights, steps=p["steps"], rebuild_every=10, dt=1.0, seed=seed,
                     description=p["desc"] if n is None else f"{p['desc']} (edge {ncell})")

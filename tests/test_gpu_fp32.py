@@ -138,15 +138,16 @@ def test_fp32_full_size_sampled():
 
 
 def test_fp32_long_rows_small_tiles():
-    """About 700 listed neighbours per atom: the 32-atom float32 tiles shrink
-    to 4096 / max_row atoms (weights scaled by 0.3 as in the float64 test)."""
+    """About 700 listed neighbours per atom: the float32 tiles shrink to what
+    their entry capacity holds (weights scaled by 0.3 as in the float64 test)."""
     rng = np.random.default_rng(31)
     hp = synth.HParams(n_species=3, cutoff=12.0, skin=0.5)
     pos, box = synth.lattice("fcc", 7, 3.6)
     pos = pos + rng.normal(0.0, 0.1, pos.shape)
     types = rng.integers(0, 3, len(pos)).astype(np.int32)
     g, _ = _compare(hp, synth.random_weights(hp, 4, 0.3), pos, types, box, "long rows")
-    assert g["stats"]["max_row"] > 600 and g["stats"]["tile_atoms"] == 4096 // g["stats"]["max_row"]
+    st = g["stats"]
+    assert st["max_row"] > 600 and 1 <= st["tile_atoms"] < 8 and st["tile_atoms"] * st["max_row"] <= 4096
 
 
 def test_fp32_md_trajectory():
