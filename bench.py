@@ -65,7 +65,10 @@ def flops_per_pair(hp) -> float:
     (2 x 2 x MAC) plus the moment and the two W contractions (6 d k)."""
     W = hp.enc_width
     mac_enc = W + (hp.enc_hidden - 1) * W * W + W * hp.k
-    d = (hp.lmax + 1) ** 2
+    if getattr(hp, "angular", 0) == 1:  # Cartesian monomials: (l+1)(l+2)/2 per order
+        d = sum((l + 1) * (l + 2) // 2 for l in range(hp.lmax + 1))
+    else:                               # irreducible harmonics: 2l+1 per order
+        d = (hp.lmax + 1) ** 2
     return 4.0 * mac_enc + 6.0 * d * hp.k
 
 
@@ -137,6 +140,20 @@ def summarize_traffic(fetch_dir: str, write_dir: str, bench_log: str, copy_bytes
                 f"see L2-to-fabric requests, which include Infinity Cache hits.\n\n")
         f.write("traffic_json: " + json.dumps(t) + "\n")
     print(json.dumps(t))
+
+
+def neighbour_build_record(events, first_ms: float, n_atoms: int, n_listed: int) -> dict:
+    """Time and bandwidth of the neighbour-list build: HIP events around the
+    rebuilds of the timed steps (the first build's wall time when none fell
+    there).  Algorithmic bytes: positions and species read (28 B per atom),
+    cell keys, permutation, sorted positions, row counts and int64 offsets
+    written (44 B per atom), 4 B per listed entry written; candidate positions
+    are re-read from cache and not counted."""
+    ms = float(np.mean([a.elapsed_time(b) for a, b in events])) if events else first_ms
+    nbytes = 72.0 * n_atoms + 4.0 * n_listed
+    return {"ms": ms, "timed_rebuilds": len(events), "algorithmic_bytes": nbytes,
+            "gbps": nbytes / (ms * 1e-3) / 1e9, "frac_of_hbm": nbytes / (ms * 1e-3) / 1e9 / PEAK_HBM_GBS,
+            "bound": "candidate scan (27 cells, about 500 distance tests per atom, twice)"}
 
 
 def capacity_sweep(edges, steps: int, seed: int, bpa: float = 450.0, precision: int = 64) -> None:
@@ -395,13 +412,20 @@ def main() -> int:
     step_no = 0
     rebuilds = 0
     compute_ms = []
+    rebuild_ms = []
 
     def md_step(timed: bool):
         nonlocal step_no, rebuilds
         step_no += 1
         d2 = pot.md_first_half(pos, vel, F, dt, ref)
         if step_no % args.rebuild_every == 0 or d2 > skin2:
+            b0 = torch.cuda.Event(enable_timing=True)
+            b1 = torch.cuda.Event(enable_timing=True)
+            b0.record(stream)
             pot.build_neighbors(pos, types, w.box)
+            b1.record(stream)
+            if timed:
+                rebuild_ms.append((b0, b1))
             ref.copy_(pos)
             rebuilds += 1
         if timed:
@@ -480,6 +504,7 @@ def main() -> int:
         "caller_bytes_per_atom": caller_bytes / N,
         "max_atoms_estimate": int(0.95 * total_mem / bpa),
         "build_ms": t_build * 1e3,
+        "neighbour_build": neighbour_build_record(rebuild_ms, t_build * 1e3, N, st["n_listed_pairs"]),
     }
     if args.cpu_sample > 0:
         log("[bench] timing the oracle on a bounded sample")
