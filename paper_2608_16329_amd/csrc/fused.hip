@@ -938,6 +938,15 @@ __device__ void head_stage(const FusedArgs& A, Smem<K, TM, R, NW, DR, NM>& S) {
     head_load(head_group(G, rw, w, NW, nin, nhid, A0f, A0Tf, hid), fnext); \
   } while (0)
 
+  // B-operand reads from the feature-major activations: element
+  // [16 (k >> 2) + drow(k & 3, g)][16 cg + c] sits at a per-lane base plus an
+  // offset that depends on k and cg only, so every read is that base with an
+  // immediate offset instead of an address register of its own
+  const R* __restrict__ xl = &S.u.hd.xT[0][0] + drow<R>(0, g) * NC + c;
+  const R* __restrict__ yl = &S.u.hd.yT[0][0] + drow<R>(0, g) * NC + c;
+  const R* __restrict__ gl = &S.u.hd.gT[0][0] + drow<R>(0, g) * NC + c;
+#define BOFF(k) ((16 * ((k) >> 2) + drow<R>((k) & 3, 0)) * NC)
+
   R* __restrict__ gbuf = kRegress ? static_cast<R*>(A.gbuf) + (long long)S.a0 * nin : nullptr;
   for (int u = tid; u < NC * nin; u += (64 * NW)) {
     const int a = u % NC, in = u / NC;
@@ -964,15 +973,14 @@ __device__ void head_stage(const FusedArgs& A, Smem<K, TM, R, NW, DR, NM>& S) {
     const int k0 = nin / 4;
     for (int kb = 0; kb < k0; kb += 16) {
       ADVANCE();
+      const R* __restrict__ xk = xl + 4 * kb * NC;  // kb is a multiple of 16
 #pragma unroll
       for (int ks = 0; ks < 16; ks += 2) {
         if (kb + ks < k0) {
-          const int k = kb + ks;
 #pragma unroll
           for (int cg = 0; cg < CG; ++cg) {
-            z0[cg] = mfma(fcur[ks], S.u.hd.xT[16 * (k >> 2) + drow<R>(k & 3, g)][16 * cg + c], z0[cg]);
-            z0b[cg] = mfma(fcur[ks + 1], S.u.hd.xT[16 * ((k + 1) >> 2) + drow<R>((k + 1) & 3, g)][16 * cg + c],
-                           z0b[cg]);
+            z0[cg] = mfma(fcur[ks], xk[BOFF(ks) + 16 * cg], z0[cg]);
+            z0b[cg] = mfma(fcur[ks + 1], xk[BOFF(ks + 1) + 16 * cg], z0b[cg]);
           }
         }
       }
@@ -1003,7 +1011,7 @@ __device__ void head_stage(const FusedArgs& A, Smem<K, TM, R, NW, DR, NM>& S) {
       for (int ks = 0; ks < 16; ++ks)
 #pragma unroll
         for (int cg = 0; cg < CG; ++cg)
-          z[cg] = mfma(fcur[ks], S.u.hd.yT[16 * (ks >> 2) + drow<R>(ks & 3, g)][16 * cg + c], z[cg]);
+          z[cg] = mfma(fcur[ks], yl[BOFF(ks) + 16 * cg], z[cg]);
     }
 #pragma unroll
     for (int cg = 0; cg < CG; ++cg) zeta[t][cg] = z[cg];
@@ -1049,7 +1057,7 @@ __device__ void head_stage(const FusedArgs& A, Smem<K, TM, R, NW, DR, NM>& S) {
       for (int ks = 0; ks < 16; ++ks)
 #pragma unroll
         for (int cg = 0; cg < CG; ++cg)
-          acc[cg] = mfma(fcur[ks], S.u.hd.gT[16 * (ks >> 2) + drow<R>(ks & 3, g)][16 * cg + c], acc[cg]);
+          acc[cg] = mfma(fcur[ks], gl[BOFF(ks) + 16 * cg], acc[cg]);
 #pragma unroll
       for (int cg = 0; cg < CG; ++cg) d[cg] += acc[cg];
     }
@@ -1075,7 +1083,7 @@ __device__ void head_stage(const FusedArgs& A, Smem<K, TM, R, NW, DR, NM>& S) {
     for (int ks = 0; ks < 16; ++ks) {
 #pragma unroll
       for (int cg = 0; cg < CG; ++cg)
-        acc[cg] = mfma(fcur[ks], S.u.hd.gT[16 * (ks >> 2) + drow<R>(ks & 3, g)][16 * cg + c], acc[cg]);
+        acc[cg] = mfma(fcur[ks], gl[BOFF(ks) + 16 * cg], acc[cg]);
     }
 #pragma unroll
     for (int cg = 0; cg < CG; ++cg) {
@@ -1093,6 +1101,7 @@ __device__ void head_stage(const FusedArgs& A, Smem<K, TM, R, NW, DR, NM>& S) {
     }
   }
   __syncthreads();
+#undef BOFF
 #undef ROW
 #undef ADVANCE
 }
