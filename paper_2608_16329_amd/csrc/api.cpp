@@ -426,7 +426,11 @@ mlip_status mlip_build_neighbors(mlip_ctx* ctx, int64_t n_atoms, const double* p
   if (flags[1] > kEntCap) return fail(ctx, MLIP_E_NBR_CAP, "a neighbour row is longer than 2048 entries");
 
   size_t need = size_t(std::max<int64_t>(total, 1));
-  if (need > ctx->cap_idx) need = need + need / 8;  // slack for later builds
+  // 1/32 headroom for later builds: in MD the list length drifts by well under
+  // that between rebuilds, and every byte of slack is a byte per entry that
+  // the largest system cannot use (the old buffer is freed before the new one
+  // is allocated, so growing never holds both)
+  if (need > ctx->cap_idx) need = need + need / 32;
   MLIP_TRY(ensure(ctx, &ctx->d_idx, &ctx->cap_idx, need, "neighbour list"));
   MLIP_HIP(ctx, launch_rows(ctx->d_spos, ctx->d_perm, n, g, ctx->d_cell_start, ctx->d_rowcnt, ctx->d_offsets,
                             ctx->d_idx, ctx->d_flags, true, s));

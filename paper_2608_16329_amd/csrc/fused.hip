@@ -941,10 +941,11 @@ __device__ void head_stage(const FusedArgs& A, Smem<K, TM, R, NW, DR, NM>& S) {
   // B-operand reads from the feature-major activations: element
   // [16 (k >> 2) + drow(k & 3, g)][16 cg + c] sits at a per-lane base plus an
   // offset that depends on k and cg only, so every read is that base with an
-  // immediate offset instead of an address register of its own
-  const R* __restrict__ xl = &S.u.hd.xT[0][0] + drow<R>(0, g) * NC + c;
-  const R* __restrict__ yl = &S.u.hd.yT[0][0] + drow<R>(0, g) * NC + c;
-  const R* __restrict__ gl = &S.u.hd.gT[0][0] + drow<R>(0, g) * NC + c;
+  // immediate offset instead of an address register of its own (no
+  // __restrict__: yT and gT are also written through S between the barriers)
+  const R* xl = &S.u.hd.xT[0][0] + drow<R>(0, g) * NC + c;
+  const R* yl = &S.u.hd.yT[0][0] + drow<R>(0, g) * NC + c;
+  const R* gl = &S.u.hd.gT[0][0] + drow<R>(0, g) * NC + c;
 #define BOFF(k) ((16 * ((k) >> 2) + drow<R>((k) & 3, 0)) * NC)
 
   R* __restrict__ gbuf = kRegress ? static_cast<R*>(A.gbuf) + (long long)S.a0 * nin : nullptr;
@@ -973,7 +974,7 @@ __device__ void head_stage(const FusedArgs& A, Smem<K, TM, R, NW, DR, NM>& S) {
     const int k0 = nin / 4;
     for (int kb = 0; kb < k0; kb += 16) {
       ADVANCE();
-      const R* __restrict__ xk = xl + 4 * kb * NC;  // kb is a multiple of 16
+      const R* xk = xl + 4 * kb * NC;  // kb is a multiple of 16
 #pragma unroll
       for (int ks = 0; ks < 16; ks += 2) {
         if (kb + ks < k0) {
