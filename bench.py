@@ -123,7 +123,7 @@ def summarize_traffic(fetch_dir: str, write_dir: str, bench_log: str, copy_bytes
                 "root on the GPU host:\n\n")
         for ctr in ("FETCH_SIZE", "WRITE_SIZE"):
             f.write(f"    cd /tmp && export TMPDIR=/tmp && timeout -s KILL 240 rocprofv3 --pmc {ctr} --kernel-trace \\\n"
-                    f"        -d <repo>/gpurun_out/<dir> -o run --output-format csv -- {command}\n\n")
+                    f"        -d <output-dir> -o run --output-format csv -- {command}\n\n")
         f.write(f"Calibration: the command first copies {copy_bytes} bytes device-to-device; that copy read "
                 f"FETCH_SIZE = {fc:.0f} KiB and WRITE_SIZE = {wc:.0f} KiB, so fetch counts are scaled by "
                 f"{f_scale:.3f} and write counts by {w_scale:.3f}.\n\n")
@@ -358,8 +358,8 @@ def main() -> int:
         return 0
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py measures one GPU only: this build has no multi-GPU path "
-              "(spatial decomposition across GPUs is described in DESIGN.md, not built)", file=sys.stderr)
+        print("bench.py measures one GPU only: the library has no multi-GPU path "
+              "(spatial decomposition across GPUs is not implemented)", file=sys.stderr)
         return 2
 
     import torch
