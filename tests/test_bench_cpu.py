@@ -29,3 +29,14 @@ def test_neighbour_build_record_without_timed_rebuilds():
     assert r["algorithmic_bytes"] == 72 * 1000 + 4 * 90_000
     assert abs(r["gbps"] - r["algorithmic_bytes"] / 0.040 / 1e9) < 1e-12
     assert abs(r["frac_of_hbm"] - r["gbps"] / bench.PEAK_HBM_GBS) < 1e-15
+
+
+def test_more_than_one_gpu_is_refused_with_a_message():
+    import os
+    import subprocess
+    import sys
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    r = subprocess.run([sys.executable, os.path.join(root, "bench.py"), "--gpus", "2"],
+                       capture_output=True, text=True, timeout=120)
+    assert r.returncode == 2
+    assert "one GPU" in r.stderr and not r.stdout.strip()
