@@ -328,6 +328,28 @@ __device__ __forceinline__ PairPos load_pair_pos(const FusedArgs& A, const Smem<
 // its ring runs further ahead.  The float32 kernel runs two wavefronts per
 // SIMD, which cover each other's load latency; there shallower rings leave
 // more registers and measured faster (ring depths 2 and 4 against 3 and 8).
+// Fragment array at a wave-uniform address, read through a buffer descriptor:
+// the descriptor and each group's offset are scalar and the lane offset is
+// one fixed vector register, so walking the array costs no vector address
+// arithmetic (which on this part would share the pipe with the float64
+// MFMAs); a read past `bytes` returns zero instead of touching other memory.
+// Group e holds one V per lane, lane l at byte (64 e + l) sizeof(V).
+constexpr int kRawBufferConfig = 0x00020000;  // raw untyped access, gfx9-family descriptor word 3
+template <typename V>
+struct FragStream {
+  __amdgpu_buffer_rsrc_t rs;
+  int lo;
+  __device__ __forceinline__ FragStream(const void* base, int bytes)
+      : rs(__builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, bytes, kRawBufferConfig)),
+        lo(int(threadIdx.x & 63) * int(sizeof(V))) {}
+  __device__ __forceinline__ V operator[](int e) const {
+    const int so = e * 64 * int(sizeof(V));
+    if constexpr (sizeof(V) == 16) return __builtin_bit_cast(V, __builtin_amdgcn_raw_buffer_load_b128(rs, lo, so, 0));
+    else if constexpr (sizeof(V) == 8) return __builtin_bit_cast(V, __builtin_amdgcn_raw_buffer_load_b64(rs, lo, so, 0));
+    else return __builtin_bit_cast(V, __builtin_amdgcn_raw_buffer_load_b32(rs, lo, so, 0));
+  }
+};
+
 template <int K, typename R>
 struct Stream {
   static constexpr int KT = K / 16;
@@ -359,7 +381,10 @@ __device__ __forceinline__ void pair_delta(const FusedArgs& A, const Smem<K, TM,
 // Encoder table of chunk ch (pair conditioning, Section 3.2).
 template <int K, int TM, typename R, int NW, int DR, int NM>
 __device__ __forceinline__ const R* chunk_table(const FusedArgs& A, const Smem<K, TM, R, NW, DR, NM>& S, int ch) {
-  const int sj = S.ch_s[ch], si = S.tile_species;
+  // the same for every lane: kept in scalar registers, so the weight loads
+  // take a scalar base and the k-step offsets cost no vector instructions
+  const int sj = __builtin_amdgcn_readfirstlane(S.ch_s[ch]);
+  const int si = __builtin_amdgcn_readfirstlane(S.tile_species);
   const int tau = A.enc_cond == 2 ? si * A.C + sj : (A.enc_cond == 1 ? sj : 0);
   return static_cast<const R*>(A.enc) + (long long)tau * A.enc_stride;
 }
@@ -389,13 +414,13 @@ __device__ __forceinline__ const R* encoder_hidden(const FusedArgs& A, const Sme
     }
   const R* __restrict__ layer = tab + 2 * kEncWidth;
   for (int t = 1; t < A.enc_hidden; ++t) {
-    const vh_t* __restrict__ frag = reinterpret_cast<const vh_t*>(layer) + lane;
+    const FragStream<vh_t> frag(layer, int(kEncWidth * kEncWidth * sizeof(R)));
     const R* __restrict__ bias = layer + kEncWidth * kEncWidth;
     vh_t wb[kRing][NH];
 #pragma unroll
     for (int p = 0; p < kRing - 1; ++p)
 #pragma unroll
-      for (int u = 0; u < NH; ++u) wb[p][u] = frag[(p * NH + u) * 64];
+      for (int u = 0; u < NH; ++u) wb[p][u] = frag[p * NH + u];
     // the forward accumulators start from the bias; the tangent has none
     v4<R> acc[8], dacc[8];
 #pragma unroll
@@ -408,7 +433,7 @@ __device__ __forceinline__ const R* encoder_hidden(const FusedArgs& A, const Sme
     for (int ks = 0; ks < 32; ++ks) {
       if (ks + kRing - 1 < 32) {
 #pragma unroll
-        for (int u = 0; u < NH; ++u) wb[(ks + kRing - 1) % kRing][u] = frag[((ks + kRing - 1) * NH + u) * 64];
+        for (int u = 0; u < NH; ++u) wb[(ks + kRing - 1) % kRing][u] = frag[(ks + kRing - 1) * NH + u];
       }
       __builtin_amdgcn_sched_barrier(0);
       const int T = ks >> 2, i = ks & 3;
@@ -454,17 +479,17 @@ __device__ __forceinline__ void encoder_out_rows(const R* __restrict__ layer, co
     b[Tc] = bout[16 * Tc + c];
     mo2[0][Tc] = mo2[1][Tc] = dmo2[0][Tc] = dmo2[1][Tc] = v4<R>{0, 0, 0, 0};
   }
-  const vo_t* __restrict__ frag = reinterpret_cast<const vo_t*>(layer) + lane;
+  const FragStream<vo_t> frag(layer, int(K * kEncWidth * sizeof(R)));
   vo_t wo[kRing][NO];
 #pragma unroll
   for (int p = 0; p < kRing - 1; ++p)
 #pragma unroll
-    for (int u = 0; u < NO; ++u) wo[p][u] = frag[(p * NO + u) * 64];
+    for (int u = 0; u < NO; ++u) wo[p][u] = frag[p * NO + u];
 #pragma unroll
   for (int ks = 0; ks < 32; ++ks) {
     if (ks + kRing - 1 < 32) {
 #pragma unroll
-      for (int u = 0; u < NO; ++u) wo[(ks + kRing - 1) % kRing][u] = frag[((ks + kRing - 1) * NO + u) * 64];
+      for (int u = 0; u < NO; ++u) wo[(ks + kRing - 1) % kRing][u] = frag[(ks + kRing - 1) * NO + u];
     }
     __builtin_amdgcn_sched_barrier(0);
     const int T = ks >> 2, i = ks & 3;
@@ -502,17 +527,17 @@ __device__ __forceinline__ void encoder_out_cols(const R* __restrict__ layer, co
                     bout[16 * Tc + drow<R>(3, g)]};
     dacc[Tc] = v4<R>{0, 0, 0, 0};
   }
-  const vo_t* __restrict__ frag = reinterpret_cast<const vo_t*>(layer) + lane;
+  const FragStream<vo_t> frag(layer, int(K * kEncWidth * sizeof(R)));
   vo_t wo[kRing][NO];
 #pragma unroll
   for (int p = 0; p < kRing - 1; ++p)
 #pragma unroll
-    for (int u = 0; u < NO; ++u) wo[p][u] = frag[(p * NO + u) * 64];
+    for (int u = 0; u < NO; ++u) wo[p][u] = frag[p * NO + u];
 #pragma unroll
   for (int ks = 0; ks < 32; ++ks) {
     if (ks + kRing - 1 < 32) {
 #pragma unroll
-      for (int u = 0; u < NO; ++u) wo[(ks + kRing - 1) % kRing][u] = frag[((ks + kRing - 1) * NO + u) * 64];
+      for (int u = 0; u < NO; ++u) wo[(ks + kRing - 1) % kRing][u] = frag[(ks + kRing - 1) * NO + u];
     }
     __builtin_amdgcn_sched_barrier(0);
     const int T = ks >> 2, i = ks & 3;
