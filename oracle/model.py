@@ -20,8 +20,8 @@ Readings of points the paper leaves open (each is stated where it is used):
   * network form: encoder h1 = silu(w0 r + b0), then (enc_hidden - 1)
     residual layers h <- h + silu(W h + b), then a linear output layer; the
     head likewise with reg_hidden hidden layers of width reg_width and a
-    linear scalar output.  SiLU and residual connections apply to both
-    networks ("SiLU activations, and residual connections");
+    linear scalar output.  The SiLU activation and the residual connections
+    apply to both networks (Section 4.1, architecture);
   * encoder input is the raw distance in Angstrom; no descriptor
     normalisation; no per-species reference energy beyond the output bias;
   * the radial feature is multiplied by the cosine cutoff
