@@ -71,7 +71,7 @@ typedef struct {
   double  skin;        /* Verlet skin in A; neighbour lists use r_c + skin       */
   int32_t k;           /* radial feature width (GPU path: 16, 32 or 64)          */
   int32_t lmax;        /* maximum angular order (GPU path: 0..5 irreducible,
-                          0..3 Cartesian; above 3 and Cartesian need k = 32)     */
+                          0..3 Cartesian; the Cartesian basis needs k = 32)      */
   int32_t angular;     /* 0 irreducible harmonic basis, d = (lmax+1)^2;
                           1 Cartesian monomials, d = (lmax+1)(lmax+2)(lmax+3)/6,
                           descriptor metric l!/(a!b!c!) (Section 3.3)            */
@@ -123,7 +123,8 @@ size_t mlip_weight_count(const mlip_hparams* hp);
  * projection tables.  hip_stream is a
  * hipStream_t (NULL = default stream); all later work is enqueued on it.
  * Errors: MLIP_E_ARG (bad hparams, unsupported on the GPU path, n_weights
- * mismatch, NULL pointers), MLIP_E_OOM, MLIP_E_HIP.  On error *out is NULL.
+ * mismatch, NULL pointers), MLIP_E_OOM, MLIP_E_HIP.  On error *out is NULL
+ * and mlip_last_error(NULL) says why.
  */
 mlip_status mlip_create(const mlip_hparams* hp, const double* weights_host, size_t n_weights,
                         void* hip_stream, mlip_ctx** out);
@@ -174,6 +175,22 @@ mlip_status mlip_compute(mlip_ctx* ctx, const double* pos_dev, double* energy_de
 mlip_status mlip_get_neighbors(mlip_ctx* ctx, int64_t* offsets_host, int32_t* idx_host);
 
 /*
+ * Copy the neighbour rows of selected atoms to the host (for checks of the
+ * list at sizes where the whole list is too large to copy; the rows are the
+ * same as those of mlip_get_neighbors).
+ *   atoms_host  int64 [n_rows], caller indices in [0, n), any order, repeats
+ *               allowed
+ *   counts_host int64 [n_rows], receives the length of each row
+ *   idx_host    int32 [cap], receives the rows back to back in the order of
+ *               atoms_host (caller indices, grouped by neighbour species)
+ * Errors: MLIP_E_ARG (NULL pointer, index outside [0, n), or the rows do not
+ * fit in cap entries: counts_host is filled even then), MLIP_E_STATE (no
+ * build), MLIP_E_HIP.  Synchronises the stream.
+ */
+mlip_status mlip_get_neighbor_rows(mlip_ctx* ctx, const int64_t* atoms_host, int64_t n_rows, int64_t* counts_host,
+                                   int32_t* idx_host, int64_t cap);
+
+/*
  * Fusion configuration of mlip_compute (Section 3.4, Table "Configurable
  * fusion"); all four give the same results up to rounding.
  *   MLIP_FUSION_CACHED     one kernel: pass 1 keeps the encoder output and its
@@ -220,7 +237,11 @@ mlip_status mlip_memory_bytes(const mlip_ctx* ctx, size_t* bytes);
 /* Fill *stats (synchronises to read the active-pair counter). */
 mlip_status mlip_get_stats(mlip_ctx* ctx, mlip_stats* stats);
 
-/* Text of the last error on this context (never NULL; "" when none). */
+/*
+ * Text of the last error on this context (never NULL; "" when none).  With
+ * ctx NULL: why the last mlip_create on the calling thread failed ("" if it
+ * succeeded).
+ */
 const char* mlip_last_error(const mlip_ctx* ctx);
 
 /* Release the context and its device memory (NULL is ignored). */

@@ -61,6 +61,14 @@ class Potential:
     def neighbors(self):
         return binding.mlip_get_neighbors(self.ctx)
 
+    def neighbor_rows(self, atoms, cap=None):
+        """Neighbour rows (caller indices) of the given atoms, one array each."""
+        atoms = np.asarray(atoms, dtype=np.int64)
+        cap = cap if cap is not None else 4096 * max(len(atoms), 1)
+        counts, idx = binding.mlip_get_neighbor_rows(self.ctx, atoms, cap)
+        ends = np.cumsum(counts)
+        return [idx[e - c:e] for c, e in zip(counts, ends)]
+
     def stats(self) -> dict:
         return binding.mlip_get_stats(self.ctx)
 

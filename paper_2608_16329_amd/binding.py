@@ -24,7 +24,8 @@ STATUS = {0: "MLIP_OK", -1: "MLIP_E_ARG", -2: "MLIP_E_OOM", -3: "MLIP_E_HIP", -4
 # Every symbol include/mlip.h declares.
 EXPORTED = ["mlip_weight_count", "mlip_create", "mlip_build_neighbors", "mlip_compute", "mlip_get_neighbors",
             "mlip_memory_bytes", "mlip_get_stats", "mlip_last_error", "mlip_destroy", "mlip_md_set_masses",
-            "mlip_md_first_half", "mlip_md_second_half", "mlip_md_kinetic", "mlip_set_fusion"]
+            "mlip_md_first_half", "mlip_md_second_half", "mlip_md_kinetic", "mlip_set_fusion",
+            "mlip_get_neighbor_rows"]
 
 MLIP_FUSION_CACHED, MLIP_FUSION_RECOMPUTE, MLIP_FUSION_PARTIAL, MLIP_FUSION_UNFUSED = 0, 1, 2, 3
 
@@ -67,6 +68,7 @@ def _load() -> ctypes.CDLL:
         "mlip_build_neighbors": (st, [vp, ctypes.c_int64, vp, vp, dp]),
         "mlip_compute": (st, [vp, vp, vp, vp, vp, dp]),
         "mlip_get_neighbors": (st, [vp, ip64, ip32]),
+        "mlip_get_neighbor_rows": (st, [vp, ip64, ctypes.c_int64, ip64, ip32, ctypes.c_int64]),
         "mlip_memory_bytes": (st, [vp, ctypes.POINTER(ctypes.c_size_t)]),
         "mlip_get_stats": (st, [vp, ctypes.POINTER(mlip_stats)]),
         "mlip_last_error": (ctypes.c_char_p, [vp]),
@@ -96,8 +98,8 @@ def _dp(a: Optional[np.ndarray]):
 
 def _check(ctx, status: int):
     if status != MLIP_OK:
-        msg = _lib.mlip_last_error(ctx).decode() if ctx else ""
-        raise MlipError(status, msg)
+        # with no context (mlip_create) the library keeps the reason per thread
+        raise MlipError(status, _lib.mlip_last_error(ctx).decode())
 
 
 def hparams_from(hp) -> mlip_hparams:
@@ -144,6 +146,18 @@ def mlip_get_neighbors(ctx: int):
     _check(ctx, _lib.mlip_get_neighbors(ctx, off.ctypes.data_as(ctypes.POINTER(ctypes.c_int64)),
                                         idx.ctypes.data_as(ctypes.POINTER(ctypes.c_int32))))
     return off, idx[:n["n_listed_pairs"]]
+
+
+def mlip_get_neighbor_rows(ctx: int, atoms, cap: int):
+    """Rows of the given atoms (caller indices): (counts int64 [n_rows], idx int32
+    [sum counts]) with cap entries of room."""
+    a = np.ascontiguousarray(atoms, dtype=np.int64)
+    counts = np.zeros(len(a), dtype=np.int64)
+    idx = np.zeros(max(int(cap), 1), dtype=np.int32)
+    _check(ctx, _lib.mlip_get_neighbor_rows(ctx, a.ctypes.data_as(ctypes.POINTER(ctypes.c_int64)), len(a),
+                                            counts.ctypes.data_as(ctypes.POINTER(ctypes.c_int64)),
+                                            idx.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)), int(cap)))
+    return counts, idx[:int(counts.sum())]
 
 
 def mlip_set_fusion(ctx: int, fusion: int) -> None:

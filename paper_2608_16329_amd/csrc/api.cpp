@@ -20,6 +20,15 @@ mlip_status fail(mlip_ctx* ctx, mlip_status st, const std::string& msg) {
   return st;
 }
 
+// Why the last mlip_create on this thread failed (there is no context to
+// hold it); mlip_last_error(NULL) returns it.
+thread_local std::string t_create_err;
+
+mlip_status create_fail(mlip_status st, const std::string& msg) {
+  t_create_err = msg;
+  return st;
+}
+
 mlip_status fail_hip(mlip_ctx* ctx, hipError_t e, const char* what) {
   (void)hipGetLastError();
   return fail(ctx, MLIP_E_HIP, std::string(what) + ": " + hipGetErrorString(e));
@@ -77,8 +86,7 @@ bool gpu_supported(const mlip_hparams* hp, std::string* why) {
   if (hp->precision != 64 && hp->precision != 32) return *why = "precision must be 64 or 32", false;
   if (hp->angular == 0 && (hp->lmax < 0 || hp->lmax > 5)) return *why = "lmax must be in 0..5 (irreducible)", false;
   if (hp->angular == 1 && (hp->lmax < 0 || hp->lmax > 3)) return *why = "lmax must be in 0..3 (Cartesian)", false;
-  if (angular_config(hp->angular, hp->lmax) != 0 && hp->k != 32)
-    return *why = "the Cartesian basis and l_max > 3 run with k = 32 only", false;
+  if (hp->angular == 1 && hp->k != 32) return *why = "the Cartesian basis runs with k = 32 only", false;
   if (hp->k != 16 && hp->k != 32 && hp->k != 64) return *why = "k must be 16, 32 or 64 on the GPU path", false;
   if (hp->enc_width != kEncWidth) return *why = "enc_width must be 128 on the GPU path", false;
   if (hp->reg_width != kHeadWidth) return *why = "reg_width must be 64 on the GPU path", false;
@@ -229,13 +237,16 @@ size_t mlip_weight_count(const mlip_hparams* hp) {
 
 mlip_status mlip_create(const mlip_hparams* hp, const double* weights_host, size_t n_weights, void* hip_stream,
                         mlip_ctx** out) {
-  if (!out) return MLIP_E_ARG;
+  t_create_err.clear();
+  if (!out) return create_fail(MLIP_E_ARG, "NULL output pointer");
   *out = nullptr;
-  if (!hp || !weights_host) return MLIP_E_ARG;
-  if (!structurally_valid(hp)) return MLIP_E_ARG;
+  if (!hp || !weights_host) return create_fail(MLIP_E_ARG, "NULL hyper-parameters or weights");
+  if (!structurally_valid(hp)) return create_fail(MLIP_E_ARG, "invalid hyper-parameters");
   std::string why;
-  if (!gpu_supported(hp, &why)) return MLIP_E_ARG;
-  if (n_weights != mlip_weight_count(hp)) return MLIP_E_ARG;
+  if (!gpu_supported(hp, &why)) return create_fail(MLIP_E_ARG, "unsupported on the GPU path: " + why);
+  if (n_weights != mlip_weight_count(hp))
+    return create_fail(MLIP_E_ARG, "n_weights is " + std::to_string(n_weights) + ", the hyper-parameters need " +
+                                       std::to_string(mlip_weight_count(hp)));
 
   mlip_ctx* ctx = new mlip_ctx();
   ctx->hp = *hp;
@@ -244,7 +255,7 @@ mlip_status mlip_create(const mlip_hparams* hp, const double* weights_host, size
       hipDeviceGetAttribute(&ctx->n_cu, hipDeviceAttributeMultiprocessorCount, ctx->device) != hipSuccess) {
     (void)hipGetLastError();
     delete ctx;
-    return MLIP_E_HIP;
+    return create_fail(MLIP_E_HIP, "no current HIP device");
   }
   const int k = hp->k;
   const int nin = (hp->lmax + 1) * k;
@@ -304,7 +315,7 @@ mlip_status mlip_create(const mlip_hparams* hp, const double* weights_host, size
       enc.size() != ctx->enc_stride * ctx->n_enc ||
       head.size() != ctx->head_stride * ctx->n_head) {
     delete ctx;
-    return MLIP_E_ARG;
+    return create_fail(MLIP_E_ARG, err.empty() ? "weight repacking size mismatch" : "angular table: " + err);
   }
   size_t cap = 0, cap2 = 0, cap3 = 0, cap4 = 0, cap5 = 0, cap6 = 0, cap7 = 0, cap8 = 0;
   mlip_status st = MLIP_OK;
@@ -317,15 +328,16 @@ mlip_status mlip_create(const mlip_hparams* hp, const double* weights_host, size
       (st = ensure(ctx, &ctx->d_flags, &cap6, size_t(4), "flags")) != MLIP_OK ||
       (st = ensure(ctx, &ctx->d_reduce, &cap7, size_t(4), "reduce")) != MLIP_OK ||
       (st = ensure(ctx, &ctx->d_inv_mass, &cap8, size_t(kMaxSpecies), "masses")) != MLIP_OK) {
+    const std::string msg = ctx->err;
     mlip_destroy(ctx);
-    return st;
+    return create_fail(st, msg);
   }
   if (upload(ctx->d_enc, enc.data(), enc.size(), eb) != hipSuccess ||
       upload(ctx->d_head, head.data(), head.size(), eb) != hipSuccess ||
       upload(ctx->d_qc, qc.data(), qc.size(), eb) != hipSuccess) {
     (void)hipGetLastError();
     mlip_destroy(ctx);
-    return MLIP_E_HIP;
+    return create_fail(MLIP_E_HIP, "weight upload failed");
   }
   *out = ctx;
   return MLIP_OK;
@@ -566,6 +578,48 @@ mlip_status mlip_get_neighbors(mlip_ctx* ctx, int64_t* offsets_host, int32_t* id
   return MLIP_OK;
 }
 
+mlip_status mlip_get_neighbor_rows(mlip_ctx* ctx, const int64_t* atoms_host, int64_t n_rows, int64_t* counts_host,
+                                   int32_t* idx_host, int64_t cap) {
+  if (!ctx) return MLIP_E_ARG;
+  ctx->err.clear();
+  if (n_rows < 0 || cap < 0) return fail(ctx, MLIP_E_ARG, "negative row count or capacity");
+  if (n_rows > 0 && (!atoms_host || !counts_host)) return fail(ctx, MLIP_E_ARG, "NULL argument");
+  if (cap > 0 && !idx_host) return fail(ctx, MLIP_E_ARG, "NULL argument");
+  if (!ctx->built) return fail(ctx, MLIP_E_STATE, "no neighbour list");
+  const int64_t n = ctx->n;
+  for (int64_t r = 0; r < n_rows; ++r)
+    if (atoms_host[r] < 0 || atoms_host[r] >= n) return fail(ctx, MLIP_E_ARG, "atom index outside [0, n)");
+  if (n_rows == 0) return MLIP_OK;
+  // sorted slot of each requested atom, by one pass over the permutation
+  // (slot -> caller index)
+  std::vector<int32_t> perm(static_cast<size_t>(n));
+  MLIP_HIP(ctx, hipStreamSynchronize(ctx->stream));
+  MLIP_HIP(ctx, hipMemcpy(perm.data(), ctx->d_perm, perm.size() * sizeof(int32_t), hipMemcpyDeviceToHost));
+  std::vector<int64_t> slot_of(static_cast<size_t>(n), -1);
+  std::vector<char> wanted(static_cast<size_t>(n), 0);
+  for (int64_t r = 0; r < n_rows; ++r) wanted[size_t(atoms_host[r])] = 1;
+  for (int64_t a = 0; a < n; ++a)
+    if (wanted[size_t(perm[size_t(a)])]) slot_of[size_t(perm[size_t(a)])] = a;
+  int64_t total = 0;
+  std::vector<int64_t> beg(static_cast<size_t>(n_rows));
+  for (int64_t r = 0; r < n_rows; ++r) {
+    int64_t off[2];
+    MLIP_HIP(ctx, hipMemcpy(off, ctx->d_offsets + slot_of[size_t(atoms_host[r])], sizeof(off), hipMemcpyDeviceToHost));
+    beg[size_t(r)] = off[0];
+    counts_host[r] = off[1] - off[0];
+    total += counts_host[r];
+  }
+  if (total > cap) return fail(ctx, MLIP_E_ARG, "the rows do not fit in cap entries");
+  int64_t at = 0;
+  for (int64_t r = 0; r < n_rows; ++r) {
+    if (counts_host[r] > 0)
+      MLIP_HIP(ctx, hipMemcpy(idx_host + at, ctx->d_idx + beg[size_t(r)], size_t(counts_host[r]) * sizeof(int32_t),
+                              hipMemcpyDeviceToHost));
+    at += counts_host[r];
+  }
+  return MLIP_OK;
+}
+
 mlip_status mlip_set_fusion(mlip_ctx* ctx, int32_t fusion) {
   if (!ctx) return MLIP_E_ARG;
   ctx->err.clear();
@@ -618,7 +672,7 @@ mlip_status mlip_get_stats(mlip_ctx* ctx, mlip_stats* st) {
 }
 
 const char* mlip_last_error(const mlip_ctx* ctx) {
-  if (!ctx) return "invalid context";
+  if (!ctx) return t_create_err.c_str();
   return ctx->err.c_str();
 }
 

@@ -1493,23 +1493,35 @@ void angular_table_shape(int acfg, int* rows, int* cols) {
 
 // Instantiations: k in {16, 32, 64}; float64 with one wavefront per SIMD,
 // float32 with two.  Atoms per tile: float64 16, float32 32 (two column
-// groups in the head), fewer where the moment tiles would not fit LDS
-// (float64 at k = 64: 8; float32 at k = 64: 16; the wider angular
-// configurations: 8 and 4 in float64, 16 and 8 in float32).  The other fusion configurations and
-// the wider angular configurations are built for k = 32.
+// groups in the head), fewer where the moment tiles would not fit LDS: at
+// k = 64 8 (float64) and 16 (float32); the Cartesian basis (k = 32) 8 and
+// 16; l_max 4..5, whose 48-row moment and 6k-wide head input grow with k,
+// 12 / 6 / 2 atoms at k = 16 / 32 / 64 in float64 and 24 / 16 / 8 in
+// float32.  The other fusion configurations are built for k = 32 with the
+// irreducible basis and l_max <= 3.
 int fused_tile_max(int k, int precision, int acfg) {
   if (acfg == 1) return precision == 64 ? 8 : 16;
-  if (acfg == 2) return precision == 64 ? 4 : 8;
+  if (acfg == 2) {
+    if (precision == 64) return k == 16 ? 12 : (k == 32 ? 6 : 2);
+    return k == 16 ? 24 : (k == 32 ? 16 : 8);
+  }
   if (precision == 64) return k == 64 ? 8 : 16;
   return k == 64 ? 16 : 32;
 }
 
 hipError_t launch_fused(int k, int precision, int acfg, int mode, const FusedArgs& a, int n_blocks, hipStream_t s) {
-  if ((mode != kCached || acfg != 0) && k != 32) return hipErrorInvalidValue;
-  if (acfg != 0 && mode != kCached) return hipErrorInvalidValue;
+  if (mode != kCached && (k != 32 || acfg != 0)) return hipErrorInvalidValue;
+  if (acfg == 1 && k != 32) return hipErrorInvalidValue;
   if (precision == 64) {
     if (acfg == 1) return launch_k<32, 8, double, 4, 32, 20, kCached>(a, n_blocks, s);
-    if (acfg == 2) return launch_k<32, 4, double, 4, 48, 56, kCached>(a, n_blocks, s);
+    if (acfg == 2) {
+      switch (k) {
+        case 16: return launch_k<16, 12, double, 4, 48, 56, kCached>(a, n_blocks, s);
+        case 32: return launch_k<32, 6, double, 4, 48, 56, kCached>(a, n_blocks, s);
+        case 64: return launch_k<64, 2, double, 4, 48, 56, kCached>(a, n_blocks, s);
+        default: return hipErrorInvalidValue;
+      }
+    }
     switch (k) {
       case 16: return launch_k<16, 16, double, 4, 16, 20, kCached>(a, n_blocks, s);
       case 32: return launch_mode<32, 16, double, 4, 16, 20>(mode, a, n_blocks, s);
@@ -1518,7 +1530,14 @@ hipError_t launch_fused(int k, int precision, int acfg, int mode, const FusedArg
     }
   } else if (precision == 32) {
     if (acfg == 1) return launch_k<32, 16, float, 8, 32, 20, kCached>(a, n_blocks, s);
-    if (acfg == 2) return launch_k<32, 8, float, 8, 48, 56, kCached>(a, n_blocks, s);
+    if (acfg == 2) {
+      switch (k) {
+        case 16: return launch_k<16, 24, float, 8, 48, 56, kCached>(a, n_blocks, s);
+        case 32: return launch_k<32, 16, float, 8, 48, 56, kCached>(a, n_blocks, s);
+        case 64: return launch_k<64, 8, float, 8, 48, 56, kCached>(a, n_blocks, s);
+        default: return hipErrorInvalidValue;
+      }
+    }
     switch (k) {
       case 16: return launch_k<16, 32, float, 8, 16, 20, kCached>(a, n_blocks, s);
       case 32: return launch_mode<32, 32, float, 8, 16, 20>(mode, a, n_blocks, s);

@@ -219,8 +219,8 @@ hipError_t launch_fill_u64(unsigned long long* p, int64_t n, hipStream_t s);
 // acfg 0 (irreducible, l_max <= 3: 16 rows x 20 monomials), 1 (Cartesian,
 // l_max <= 3: 32 x 20) or 2 (irreducible, l_max 4..5: 48 x 56); mode 0
 // cached, 1 recompute, 2 encoding, 3 regression, 4 derivation kernel of the
-// three-kernel split.  Configurations other than acfg 0 / mode 0 exist for
-// k = 32, and acfg 1, 2 only with mode 0.
+// three-kernel split.  Modes other than 0 exist for k = 32 with acfg 0, and
+// acfg 1 for k = 32.
 int angular_config(int angular, int lmax);
 void angular_table_shape(int acfg, int* rows, int* cols);
 int fused_tile_max(int k, int precision, int acfg);  // centre atoms per tile of that instantiation

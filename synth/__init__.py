@@ -120,6 +120,20 @@ def random_weights(hp: HParams, seed: int, scale: float = 1.0, energy_scale: flo
     return np.concatenate(parts).astype(np.float64)
 
 
+def scale_segments(hp: HParams, weights: np.ndarray, suffix: str, factor: float) -> np.ndarray:
+    """Copy of a weight blob with every segment whose name ends in `suffix`
+    (for example ".A0", the head's first layer in each head table)
+    multiplied by `factor`."""
+    out = np.array(weights, dtype=np.float64, copy=True)
+    pos = 0
+    for name, n, _ in weight_segments(hp):
+        if name.endswith(suffix):
+            out[pos:pos + n] *= factor
+        pos += n
+    assert pos == len(out)
+    return out
+
+
 def lattice(kind: str, n: int, a: float) -> Tuple[np.ndarray, np.ndarray]:
     """Cubic n x n x n supercell of an FCC or BCC lattice, sites ordered
     (ix, iy, iz, basis).  Returns positions [N][3] and the box edges."""

@@ -1,10 +1,16 @@
 """GPU parity of the float32 network path (mlip_hparams.precision = 32)
 against the float64 oracle on identical seeded inputs.
 
-The bar is relative: for each output array (E_i, F, per-atom virial) the
-largest absolute deviation from the oracle must stay within 1e-4 of that
-array's largest oracle magnitude.  Neighbour sets do not depend on the
-network precision and must be identical."""
+The bar is relative, in two parts, for each output array (E_i, F, per-atom
+virial):
+  * normwise: the largest absolute deviation from the oracle stays within
+    1e-4 of the array's largest oracle magnitude;
+  * per element: every entry whose oracle magnitude is at least a tenth of
+    the array's largest deviates by at most 1e-4 of its own magnitude.
+Smaller entries are sums whose terms cancel, and float32 rounding of those
+terms is relative to the terms, not to the sum; their per-element figures
+(floors 1e-2 and 1e-3 of the largest) are logged.  Neighbour sets do not
+depend on the network precision and must be identical."""
 import dataclasses
 
 import numpy as np
@@ -14,16 +20,41 @@ import synth
 import oracle
 from oracle.model import Model, evaluate
 from oracle.neighbors import neighbor_list
-from tests.gpu_helpers import gpu_eval, assert_same_neighbor_sets, max_abs, log, oracle_sample, to_dev
+from tests.gpu_helpers import (gpu_eval, assert_same_neighbor_sets, max_abs, log, oracle_sample, to_dev,
+                               curved_head, oracle_cube)
 
 pytestmark = pytest.mark.gpu
 
 REL_TOL = 1e-4
+ELEM_FLOOR = 0.1   # per-element check for entries at least this fraction of the array's largest
 
 
 def rel_err(a, ref):
     scale = float(np.max(np.abs(ref)))
     return max_abs(a, ref) / scale if scale > 0 else max_abs(a, ref)
+
+
+def elem_rel(a, ref, floor):
+    """Largest per-element relative deviation over the entries whose oracle
+    magnitude is at least `floor` times the array's largest."""
+    a, ref = np.asarray(a).ravel(), np.asarray(ref).ravel()
+    scale = float(np.max(np.abs(ref))) if ref.size else 0.0
+    m = np.abs(ref) >= floor * scale
+    if scale == 0.0 or not m.any():
+        return 0.0
+    return float(np.max(np.abs(a[m] - ref[m]) / np.abs(ref[m])))
+
+
+def check_elementwise(label, pairs):
+    """Log the per-element figures at three floors and assert the bar at
+    ELEM_FLOOR."""
+    parts = []
+    for key, a, ref in pairs:
+        parts.append(key + " " + " ".join(f"{f:g}:{elem_rel(a, ref, f):.1e}" for f in (0.1, 0.01, 0.001)))
+    log(f"[fp32] {label}: per-element rel (floor:value) " + "; ".join(parts))
+    for key, a, ref in pairs:
+        e = elem_rel(a, ref, ELEM_FLOOR)
+        assert e <= REL_TOL, (key, e)
 
 
 def _hp32(hp):
@@ -41,6 +72,7 @@ def _compare(hp, weights, pos, types, box, label):
     ref = evaluate(m, pos, types, box, off, idx)
     eE, eF, eV = rel_err(g["E_i"], ref["E_i"]), rel_err(g["F"], ref["F"]), rel_err(g["virial"], ref["virial"])
     log(f"[fp32] {label}: rel dE={eE:.2e} dF={eF:.2e} dW={eV:.2e}")
+    check_elementwise(label, [("E", g["E_i"], ref["E_i"]), ("F", g["F"], ref["F"]), ("W", g["virial"], ref["virial"])])
     assert eE <= REL_TOL, eE
     assert eF <= REL_TOL, eF
     assert eV <= REL_TOL, eV
@@ -62,8 +94,27 @@ VARIANTS = {
     "k16": {"k": 16},
     "k64": {"k": 64},
     "cartesian": {"angular": 1},
+    "lmax4": {"lmax": 4},
     "lmax5": {"lmax": 5},
+    "k16_lmax5": {"k": 16, "lmax": 5},
+    "k64_lmax4": {"k": 64, "lmax": 4},
+    "k64_lmax5": {"k": 64, "lmax": 5},
 }
+
+
+@pytest.mark.parametrize("name,n,over", [("fcc-binary-4", None, {}), ("fcc-hea6-128", 5, {}),
+                                         ("fcc-binary-4", None, {"enc_hidden": 5, "reg_hidden": 6})])
+def test_fp32_head_in_curved_region(name, n, over):
+    """The head's first layer scaled so most head pre-activations lie where
+    the SiLU curves (|z| < 4): the float32 sigmoid (hardware exp2 and
+    reciprocal) and its backward factor away from the saturated branches."""
+    w = synth.make_workload(name, seed=3, n=n, hp_overrides=over)
+    wts, frac = curved_head(w.hp, w.weights, w.pos, w.types, w.box)
+    log(f"[fp32] {name}/curved head {over}: fraction |z| < 4 per head layer {[round(f, 2) for f in frac]}")
+    # most units curved: the first head layer, and the layers on average (deep
+    # residual stacks drift outwards in their last layers)
+    assert frac[0] > 0.5 and float(np.mean(frac)) > 0.5, frac
+    _compare(w.hp, wts, w.pos, w.types, w.box, f"{name}/curved head {over}")
 
 
 @pytest.mark.parametrize("variant", list(VARIANTS))
@@ -111,7 +162,8 @@ def test_fp32_agrees_with_fp64_path():
 
 def test_fp32_full_size_sampled():
     """8,388,608-atom 6-component FCC in the launch configuration of the
-    benchmark, float32 network: sampled atoms against the oracle."""
+    benchmark, float32 network: a corner cube of 2,456 lattice sites against
+    the oracle."""
     import torch
     from paper_2608_16329_amd import Potential
     w = synth.make_workload("fcc-hea6-128", seed=0, hp_overrides={"precision": 32})
@@ -126,13 +178,14 @@ def test_fp32_full_size_sampled():
     V = torch.empty((N, 9), dtype=torch.float64, device="cuda:0")
     pot.compute(p, F, E, V)
     torch.cuda.synchronize()
-    rng = np.random.default_rng(12)
-    atoms = rng.choice(N, 48, replace=False)
     m = Model(w.hp, w.weights)
-    Er, Fr, Vr = oracle_sample(m, w.pos, w.types, w.box, atoms)
+    log("[fp32] full size: oracle on a corner cube")
+    atoms, Er, Fr, Vr = oracle_cube(m, w.pos, w.types, w.box, np.zeros(3), 15.5)
+    assert len(atoms) >= 2000
     Eg, Fg, Vg = E.cpu().numpy()[atoms], F.cpu().numpy()[atoms], V.cpu().numpy()[atoms]
     eE, eF, eV = rel_err(Eg, Er), rel_err(Fg, Fr), rel_err(Vg, Vr)
-    log(f"[fp32] full size sampled: rel dE={eE:.2e} dF={eF:.2e} dW={eV:.2e}")
+    log(f"[fp32] full size, {len(atoms)} atoms: rel dE={eE:.2e} dF={eF:.2e} dW={eV:.2e}")
+    check_elementwise("full size", [("E", Eg, Er), ("F", Fg, Fr), ("W", Vg, Vr)])
     assert eE <= REL_TOL and eF <= REL_TOL and eV <= REL_TOL
     pot.close()
 
@@ -176,4 +229,5 @@ def test_fp32_md_trajectory():
         e = rel_err(F.cpu().numpy(), r["F"])
         log(f"[fp32] md step {step}: rel dF={e:.2e}")
         assert e <= REL_TOL
+        check_elementwise(f"md step {step}", [("F", F.cpu().numpy(), r["F"])])
     pot.close()

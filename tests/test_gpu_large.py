@@ -1,153 +1,258 @@
 """GPU parity at the full workload sizes, in the launch configuration the
-benchmark times (same library calls, persistent grid over all CUs):
-sampled atoms are checked against the oracle one by one (each from a local
-cluster cut out of the periodic system), sampled neighbour rows against the
-oracle's brute-force rows over all N atoms."""
+benchmark times (same library calls, persistent grid over all CUs).
+
+The oracle checks cubes of thousands of atoms of the periodic system (each
+cube cut out with every centre whose partial forces reach its atoms, the
+centres spread over worker processes on the host cores), or the whole
+system where it is small enough; neighbour rows of thousands of atoms are
+compared as sets, bit for bit, against the exact definition applied to the
+caller's coordinates.  MD runs use the head-output scale of the benchmark
+(forces of a trained potential's size); step-0 checks use the unscaled
+weights, whose larger forces make the same absolute tolerance stricter."""
 import numpy as np
 import pytest
 
 import synth
 from oracle.model import Model
-from oracle.neighbors import neighbors_of
-from tests.gpu_helpers import to_dev, oracle_sample, log, max_abs
+from tests.gpu_helpers import (to_dev, log, max_abs, oracle_cube, oracle_full, cube_members, oracle_rows,
+                               compare_rows)
 
 pytestmark = pytest.mark.gpu
 
 TOL = 1e-9
 
 
-def _run(name, n_sample, seed=0):
+def _outputs(N):
     import torch
-    from paper_2608_16329_amd import Potential
-    log(f"[large] {name}: generating")
-    w = synth.make_workload(name, seed=seed)
-    N = len(w.pos)
     dev = torch.device("cuda:0")
+    return (torch.zeros((N, 3), dtype=torch.float64, device=dev), torch.zeros(N, dtype=torch.float64, device=dev),
+            torch.zeros((N, 9), dtype=torch.float64, device=dev))
+
+
+def _check_cube(label, pot, m, pos_h, types_h, box, F, E, V, centre, half, n_rows, index=None):
+    """E_i, F_i and virial of every atom in the cube against the oracle, and
+    the neighbour rows of n_rows of them bit for bit.  pos_h/types_h: the
+    system or a subset holding every atom within reach (global indices in
+    `index`)."""
+    import torch
+    rl = m.rc + m.skin
+    index = np.arange(len(pos_h)) if index is None else np.asarray(index)
+    log(f"[large] {label}: oracle on the cube of half-edge {half} A around {np.round(centre, 2).tolist()}")
+    atoms, oE, oF, oV = oracle_cube(m, pos_h, types_h, box, centre, half, index=index)
+    sel = torch.from_numpy(atoms).to(F.device)
+    gE, gF, gV = E[sel].cpu().numpy(), F[sel].cpu().numpy(), V[sel].cpu().numpy()
+    eE, eF, eV = max_abs(gE, oE), max_abs(gF, oF), max_abs(gV, oV)
+    log(f"[large] {label}: {len(atoms)} atoms, max|dE|={eE:.3e} max|dF|={eF:.3e} max|dW|={eV:.3e} "
+        f"(|F|max={np.abs(oF).max():.2f})")
+    assert len(atoms) >= 2000
+    assert eE <= TOL and eF <= TOL and eV <= TOL, (eE, eF, eV)
+    # rows: spread over the cube; the exact definition is applied to the
+    # atoms within r_c + skin + 1 of the cube (global indices ascending)
+    step = max(1, len(atoms) // n_rows)
+    rows = atoms[::step][:n_rows]
+    sub = cube_members(pos_h, box, centre, half + rl + 1.0)
+    gsub = index[sub]
+    loc = np.searchsorted(gsub, rows)
+    assert np.array_equal(gsub[loc], rows)
+    ref = [gsub[r] for r in oracle_rows(pos_h[sub], box, rl, loc)]
+    got = pot.neighbor_rows(rows)
+    compare_rows(got, ref, rows)
+    log(f"[large] {label}: {len(rows)} neighbour rows identical")
+    return len(atoms), len(rows)
+
+
+def _totals_and_momentum(tot, F, E, V):
+    Et = E.sum().item()
+    assert abs(tot[0] - Et) <= 1e-8 * max(1.0, abs(Et))
+    Wt = V.sum(0).cpu().numpy()
+    assert np.abs(tot[1:] - Wt).max() <= 1e-8 * max(1.0, np.abs(Wt).max())
+    Fs = F.sum(0).cpu().numpy()
+    assert np.abs(Fs).max() <= 1e-12 * F.shape[0] * F.abs().max().item()
+
+
+def _md(pot, pos, vel, types, F, E, V, box, skin, steps, first_step=1):
+    """Velocity-Verlet steps on the GPU with the benchmark's rebuild rule."""
+    import torch
+    ref = pos.clone()
+    for s in range(first_step, first_step + steps):
+        d2 = pot.md_first_half(pos, vel, F, 1.0, ref)
+        if s % 10 == 0 or d2 > (0.5 * skin) ** 2:
+            pot.build_neighbors(pos, types, box)
+            ref.copy_(pos)
+        pot.compute(pos, F, E, V)
+        pot.md_second_half(vel, F, 1.0)
+        if s % 10 == 0:
+            torch.cuda.synchronize()
+            log(f"[large] md step {s}")
+    torch.cuda.synchronize()
+
+
+def test_six_component_fcc_8m_cube_step0():
+    """8,388,608-atom six-component FCC: a corner cube of 12,194 lattice sites
+    (it straddles every periodic face) and 2,000 of its rows."""
+    from paper_2608_16329_amd import Potential
+    w = synth.make_workload("fcc-hea6-128", seed=0)
+    N = len(w.pos)
     pot = Potential(w.hp, w.weights)
-    pos = to_dev(w.pos)
-    types = to_dev(w.types)
-    F = torch.empty((N, 3), dtype=torch.float64, device=dev)
-    E = torch.empty(N, dtype=torch.float64, device=dev)
-    V = torch.empty((N, 9), dtype=torch.float64, device=dev)
-    log(f"[large] {name}: N={N} build + compute")
+    pos, types = to_dev(w.pos), to_dev(w.types)
+    F, E, V = _outputs(N)
+    log(f"[large] fcc-hea6-128 N={N}: build + compute")
     pot.build_neighbors(pos, types, w.box)
     tot = pot.compute(pos, F, E, V, totals=True)
-    torch.cuda.synchronize()
-    st = pot.stats()
-    rng = np.random.default_rng(seed + 7)
-    atoms = list(rng.choice(N, n_sample - 4, replace=False)) + [0, N - 1]
-    for s in range(w.hp.n_species):       # one atom of each species, the rarest first
-        idx = np.nonzero(w.types == s)[0]
-        if len(idx):
-            atoms.append(int(idx[len(idx) // 2]))
-    atoms = sorted(set(int(a) for a in atoms))
-    m = Model(w.hp, w.weights)
-    log(f"[large] {name}: oracle on {len(atoms)} sampled atoms")
-    oE, oF, oV = oracle_sample(m, w.pos, w.types, w.box, atoms)
-    gE = E[atoms].cpu().numpy()
-    gF = F[atoms].cpu().numpy()
-    gV = V[atoms].cpu().numpy()
-    eE, eF, eV = np.abs(gE - oE).max(), np.abs(gF - oF).max(), np.abs(gV - oV).max()
-    log(f"[large] {name}: max|dE|={eE:.3e} max|dF|={eF:.3e} max|dW|={eV:.3e}")
-    assert eE <= TOL and eF <= TOL and eV <= TOL
-    # totals are the sums of the per-atom outputs
-    Et = E.sum().item()
-    assert abs(tot[0] - Et) <= 1e-9 * max(1.0, abs(Et)) * 10
-    Wt = V.sum(0).cpu().numpy()
-    assert np.abs(tot[1:] - Wt).max() <= 1e-9 * max(1.0, np.abs(Wt).max()) * 10
-    # momentum: sum of forces vanishes up to rounding
-    Fs = F.sum(0).cpu().numpy()
-    assert np.abs(Fs).max() <= 1e-12 * N * F.abs().max().item()
-    # neighbour rows of a few atoms, bit for bit
-    log(f"[large] {name}: neighbour rows")
-    goff, gidx = pot.neighbors()
-    rl = w.hp.cutoff + w.hp.skin
-    rows = atoms[:6]
-    ref = neighbors_of(w.pos, w.box, rl, rows)
-    for a, r in zip(rows, ref):
-        assert np.array_equal(np.sort(gidx[goff[a]:goff[a + 1]]), r), a
-    assert st["n_listed_pairs"] == goff[-1]
+    _totals_and_momentum(tot, F, E, V)
+    n_atoms, _ = _check_cube("fcc-hea6-128 step 0", pot, Model(w.hp, w.weights), w.pos, w.types, w.box,
+                             F, E, V, np.zeros(3), 26.0, 2000)
+    assert n_atoms >= 10000
     pot.close()
 
 
-def test_six_component_fcc_8m_sampled():
-    _run("fcc-hea6-128", 14)
-
-
-def test_ternary_fcc_1m_sampled():
-    _run("fcc-ternary-64", 12)
-
-
-def test_bcc_unary_nve_100_steps_sampled():
-    """100 NVE steps of the 65,536-atom BCC metal on the GPU (rebuild every
-    10 steps or on the skin guard); at steps 10, 50 and 100 the oracle is
-    fed the GPU's own positions for sampled atoms."""
-    import torch
+def test_six_component_fcc_8m_cube_after_md():
+    """The same alloy after 10 NVE steps (rebuild at step 10), positions taken
+    from the GPU: a cube of about 12,200 atoms at the box centre."""
     from paper_2608_16329_amd import Potential
-    w = synth.make_workload("bcc-unary-32", seed=3)
+    w = synth.make_workload("fcc-hea6-128", seed=1, energy_scale=synth.PHYSICAL_ENERGY_SCALE)
+    N = len(w.pos)
+    pot = Potential(w.hp, w.weights)
+    pot.set_masses(w.masses)
+    pos, vel, types = to_dev(w.pos), to_dev(w.vel), to_dev(w.types)
+    F, E, V = _outputs(N)
+    pot.build_neighbors(pos, types, w.box)
+    pot.compute(pos, F, E, V)
+    _md(pot, pos, vel, types, F, E, V, w.box, w.hp.skin, 10)
+    assert pot.stats()["n_builds"] == 2
+    p = pos.cpu().numpy()
+    n_atoms, _ = _check_cube("fcc-hea6-128 step 10", pot, Model(w.hp, w.weights), p, w.types, w.box,
+                             F, E, V, w.box / 2.0, 26.0, 2000)
+    assert n_atoms >= 10000
+    pot.close()
+
+
+def test_ternary_fcc_1m_md_steps_0_50_100():
+    """1,048,576-atom dilute ternary FCC, 100 NVE steps at 600 K: cubes of
+    more than 2,000 atoms at steps 0, 50 and 100."""
+    from paper_2608_16329_amd import Potential
+    w = synth.make_workload("fcc-ternary-64", seed=2, energy_scale=synth.PHYSICAL_ENERGY_SCALE)
     N = len(w.pos)
     m = Model(w.hp, w.weights)
     pot = Potential(w.hp, w.weights)
     pot.set_masses(w.masses)
     pos, vel, types = to_dev(w.pos), to_dev(w.vel), to_dev(w.types)
-    ref = pos.clone()
-    dev = torch.device("cuda:0")
-    F = torch.zeros((N, 3), dtype=torch.float64, device=dev)
-    E = torch.zeros(N, dtype=torch.float64, device=dev)
-    V = torch.zeros((N, 9), dtype=torch.float64, device=dev)
+    F, E, V = _outputs(N)
     pot.build_neighbors(pos, types, w.box)
     pot.compute(pos, F, E, V)
-    rng = np.random.default_rng(5)
-    rebuilds = 0
-    for step in range(1, 101):
-        d2 = pot.md_first_half(pos, vel, F, 1.0, ref)
-        if step % 10 == 0 or d2 > (0.5 * w.hp.skin) ** 2:
-            pot.build_neighbors(pos, types, w.box)
-            ref.copy_(pos)
-            rebuilds += 1
-        pot.compute(pos, F, E, V)
-        pot.md_second_half(vel, F, 1.0)
-        if step in (10, 50, 100):
-            torch.cuda.synchronize()
-            p = pos.cpu().numpy()
-            atoms = sorted(int(a) for a in rng.choice(N, 6, replace=False))
-            oE, oF, oV = oracle_sample(m, p, w.types, w.box, atoms)
-            eE = np.abs(E[atoms].cpu().numpy() - oE).max()
-            eF = np.abs(F[atoms].cpu().numpy() - oF).max()
-            eV = np.abs(V[atoms].cpu().numpy() - oV).max()
-            log(f"[md] step {step}: rebuilds {rebuilds} max|dE|={eE:.3e} max|dF|={eF:.3e} max|dW|={eV:.3e}")
-            assert eE <= TOL and eF <= TOL and eV <= TOL
-            goff, gidx = pot.neighbors()
-            ref_rows = neighbors_of(p, w.box, w.hp.cutoff + w.hp.skin, atoms[:3])
-            for a, r in zip(atoms[:3], ref_rows):
-                assert np.array_equal(np.sort(gidx[goff[a]:goff[a + 1]]), r)
+    # cubes centred on lattice sites: 2,457 sites each
+    centres = {0: np.zeros(3), 50: np.full(3, 21 * 4.05), 100: np.full(3, 45 * 4.05)}
+    _check_cube("fcc-ternary-64 step 0", pot, m, w.pos, w.types, w.box, F, E, V, centres[0], 17.0, 2000)
+    _md(pot, pos, vel, types, F, E, V, w.box, w.hp.skin, 50, 1)
+    _check_cube("fcc-ternary-64 step 50", pot, m, pos.cpu().numpy(), w.types, w.box, F, E, V, centres[50], 17.0,
+                2000)
+    _md(pot, pos, vel, types, F, E, V, w.box, w.hp.skin, 50, 51)
+    _check_cube("fcc-ternary-64 step 100", pot, m, pos.cpu().numpy(), w.types, w.box, F, E, V, centres[100],
+                17.0, 2000)
     pot.close()
 
 
-def test_bcc_six_component_sweep_shape_sampled():
-    """The capacity-sweep alloy (6-component BCC, a = 3.2 A) at L = 128
-    (4,194,304 atoms) in the launch configuration of the sweep: sampled
-    atoms against the oracle."""
+def test_bcc_unary_65k_full_md_steps_0_50_100():
+    """65,536-atom BCC metal, 100 NVE steps: the whole system (every E_i, F_i,
+    virial and neighbour row) against the oracle at steps 0, 50 and 100."""
+    from paper_2608_16329_amd import Potential
+    w = synth.make_workload("bcc-unary-32", seed=3, energy_scale=synth.PHYSICAL_ENERGY_SCALE)
+    N = len(w.pos)
+    m = Model(w.hp, w.weights)
+    pot = Potential(w.hp, w.weights)
+    pot.set_masses(w.masses)
+    pos, vel, types = to_dev(w.pos), to_dev(w.vel), to_dev(w.types)
+    F, E, V = _outputs(N)
+    pot.build_neighbors(pos, types, w.box)
+    tot = pot.compute(pos, F, E, V, totals=True)
+    for step in (0, 50, 100):
+        if step:
+            _md(pot, pos, vel, types, F, E, V, w.box, w.hp.skin, 50, step - 49)
+            tot = pot.compute(pos, F, E, V, totals=True)
+        p = pos.cpu().numpy()
+        log(f"[large] bcc-unary-32 step {step}: oracle on all {N} atoms")
+        oE, oF, oV, off, idx = oracle_full(m, p, w.types, w.box)
+        eE = max_abs(E.cpu().numpy(), oE)
+        eF = max_abs(F.cpu().numpy(), oF)
+        eV = max_abs(V.cpu().numpy(), oV)
+        log(f"[large] bcc-unary-32 step {step}: max|dE|={eE:.3e} max|dF|={eF:.3e} max|dW|={eV:.3e}")
+        assert eE <= TOL and eF <= TOL and eV <= TOL
+        assert abs(tot[0] - oE.sum()) <= TOL * N
+        goff, gidx = pot.neighbors()
+        # the GPU list was built at the last rebuild, the oracle's now: both are
+        # valid lists, equal when the build was at this step
+        if step % 10 == 0:
+            compare_rows([gidx[goff[i]:goff[i + 1]] for i in range(N)], [idx[off[i]:off[i + 1]] for i in range(N)],
+                         range(N))
+            log(f"[large] bcc-unary-32 step {step}: all {N} neighbour rows identical")
+    pot.close()
+
+
+def test_bcc_sweep_edge_l384_list_beyond_2_31_entries():
+    """The capacity-sweep alloy (six-component BCC, a = 3.2 A) at L = 384:
+    113,246,208 atoms whose neighbour list holds about 7.1e9 entries, beyond
+    the 2^31 of a 32-bit offset.  A cube of more than 2,000 atoms and 2,000
+    rows against the oracle, with only the atoms near the cube copied to the
+    host."""
     import torch
+    from paper_2608_16329_amd import Potential
+    p = synth.PRESETS["bcc-hea6-sweep"]
+    L = 384
+    N = 2 * L ** 3
+    hp = synth.HParams(n_species=p["C"], cutoff=p["cutoff"], skin=0.5)
+    weights = synth.random_weights(hp, 1)
+    masses = np.array([synth.MASS[x] for x in p["masses"]])
+    box = np.array([L * p["a"]] * 3)
+    dev = torch.device("cuda:0")
+    pos = torch.empty((N, 3), dtype=torch.float64, device=dev)
+    types = torch.empty(N, dtype=torch.int32, device=dev)
+    for first, cp, ct, _ in synth.lattice_stream("bcc", L, p["a"], p["C"], p["sigma"], masses, p["T"], 0):
+        m_ = len(cp)
+        if (first // m_) % 6 == 0:
+            log(f"[large] L={L}: generating, {first}/{N} sites")
+        pos[first:first + m_] = torch.from_numpy(cp).to(dev)
+        types[first:first + m_] = torch.from_numpy(ct).to(dev)
+    pot = Potential(hp, weights)
+    log(f"[large] L={L} N={N}: build")
+    pot.build_neighbors(pos, types, box)
+    st = pot.stats()
+    log(f"[large] L={L}: {st['n_listed_pairs']} listed entries")
+    assert st["n_listed_pairs"] > 2 ** 31
+    F, E, V = _outputs(N)
+    log(f"[large] L={L}: compute")
+    pot.compute(pos, F, E, V)
+    torch.cuda.synchronize()
+    centre = np.array([142.0, 200.0, 311.0]) * p["a"]   # a lattice site deep inside, not at an end of the order
+    half = 16.5
+    m = Model(hp, weights)
+    reach = half + 2.0 * (m.rc + m.skin) + 1.0
+    c = torch.from_numpy(centre).to(dev)
+    bt = torch.from_numpy(box).to(dev)
+    d = pos - c
+    d -= bt * torch.round(d / bt)
+    near = torch.nonzero((d.abs() < reach).all(dim=1)).squeeze(1)
+    del d
+    index = near.cpu().numpy()
+    _check_cube(f"bcc sweep L={L}", pot, m, pos[near].cpu().numpy(), types[near].cpu().numpy(), box, F, E, V,
+                centre, half, 2000, index=index)
+    pot.close()
+    del pos, types, F, E, V
+    torch.cuda.empty_cache()
+
+
+def test_bcc_sweep_shape_l128_cube():
+    """The capacity-sweep alloy at L = 128 (4,194,304 atoms): a corner cube
+    of more than 2,000 atoms and 2,000 rows."""
     from paper_2608_16329_amd import Potential
     w = synth.make_workload("bcc-hea6-sweep", seed=0, n=128)
     N = len(w.pos)
-    log(f"[large] bcc sweep shape N={N}")
     pot = Potential(w.hp, w.weights)
-    p = to_dev(w.pos)
-    pot.build_neighbors(p, to_dev(w.types), w.box)
-    F = torch.empty((N, 3), dtype=torch.float64, device="cuda:0")
-    E = torch.empty(N, dtype=torch.float64, device="cuda:0")
-    V = torch.empty((N, 9), dtype=torch.float64, device="cuda:0")
-    pot.compute(p, F, E, V)
-    torch.cuda.synchronize()
-    atoms = np.random.default_rng(21).choice(N, 32, replace=False)
-    Er, Fr, Vr = oracle_sample(Model(w.hp, w.weights), w.pos, w.types, w.box, atoms)
-    eE = max_abs(E.cpu().numpy()[atoms], Er)
-    eF = max_abs(F.cpu().numpy()[atoms], Fr)
-    eV = max_abs(V.cpu().numpy()[atoms], Vr)
-    log(f"[large] bcc sweep shape: max|dE|={eE:.2e} max|dF|={eF:.2e} max|dW|={eV:.2e}")
-    assert max(eE, eF, eV) <= 1e-9
+    pos = to_dev(w.pos)
+    pot.build_neighbors(pos, to_dev(w.types), w.box)
+    F, E, V = _outputs(N)
+    pot.compute(pos, F, E, V)
+    _check_cube("bcc sweep L=128", pot, Model(w.hp, w.weights), w.pos, w.types, w.box, F, E, V, np.zeros(3),
+                16.5, 2000)
     pot.close()
 
 

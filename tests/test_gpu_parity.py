@@ -8,7 +8,7 @@ import synth
 import oracle
 from oracle.model import Model, evaluate
 from oracle.neighbors import brute_force_neighbors, neighbor_list
-from tests.gpu_helpers import gpu_eval, to_dev, assert_same_neighbor_sets, max_abs, log
+from tests.gpu_helpers import gpu_eval, to_dev, assert_same_neighbor_sets, max_abs, log, curved_head
 
 pytestmark = pytest.mark.gpu
 
@@ -68,6 +68,11 @@ VARIANTS = {
     "cartesian_lmax2_universal": {"angular": 1, "lmax": 2, "enc_cond": 0},
     "lmax4": {"lmax": 4},
     "lmax5": {"lmax": 5},
+    "k16_lmax4": {"k": 16, "lmax": 4},
+    "k16_lmax5": {"k": 16, "lmax": 5},
+    "k64_lmax4": {"k": 64, "lmax": 4},
+    "k64_lmax5": {"k": 64, "lmax": 5},
+    "k64_lmax5_deep_universal": {"k": 64, "lmax": 5, "enc_hidden": 4, "reg_hidden": 3, "enc_cond": 0},
 }
 
 
@@ -77,6 +82,23 @@ def test_binary_fcc_variants(variant):
     _compare(w.hp, w.weights, w.pos, w.types, w.box, f"fcc-binary-4/{variant}")
 
 
+@pytest.mark.parametrize("name,n,over", [("fcc-binary-4", None, {}), ("fcc-hea6-128", 5, {}),
+                                         ("fcc-binary-4", None, {"enc_hidden": 5, "reg_hidden": 6}),
+                                         ("fcc-binary-4", None, {"lmax": 5, "k": 16})])
+def test_head_in_curved_region(name, n, over):
+    """The head's first layer scaled so that most pre-activations of every
+    head layer lie where the SiLU and its derivative curve (|z| < 4), which
+    exercises the sigmoid and the backward factor s (1 + z (1 - s)) away
+    from their saturated branches."""
+    w = synth.make_workload(name, seed=3, n=n, hp_overrides=over)
+    wts, frac = curved_head(w.hp, w.weights, w.pos, w.types, w.box)
+    log(f"[parity] {name}/curved head {over}: fraction |z| < 4 per head layer {[round(f, 2) for f in frac]}")
+    # most units curved: the first head layer, and the layers on average (deep
+    # residual stacks drift outwards in their last layers)
+    assert frac[0] > 0.5 and float(np.mean(frac)) > 0.5, frac
+    _compare(w.hp, wts, w.pos, w.types, w.box, f"{name}/curved head {over}")
+
+
 @pytest.mark.parametrize("name,n", [("fcc-ternary-64", 4), ("fcc-hea6-128", 5), ("bcc-unary-32", 6),
                                     ("bcc-hea6-sweep", 5)])
 def test_preset_shapes(name, n):
@@ -84,10 +106,10 @@ def test_preset_shapes(name, n):
     _compare(w.hp, w.weights, w.pos, w.types, w.box, f"{name}/n={n}")
 
 
-@pytest.mark.parametrize("over", [{"angular": 1}, {"lmax": 5}])
+@pytest.mark.parametrize("over", [{"angular": 1}, {"lmax": 5}, {"lmax": 5, "k": 16}, {"lmax": 4, "k": 64}])
 def test_angular_sweep_six_species(over):
-    """The Cartesian d = 20 basis and l_max = 5 (d = 36) on the 6-component
-    FCC shape (several angular row tiles, multi-tile moments)."""
+    """The Cartesian d = 20 basis and l_max = 4, 5 (d = 25, 36) on the
+    6-component FCC shape (several angular row tiles, multi-tile moments)."""
     w = synth.make_workload("fcc-hea6-128", seed=8, n=5, hp_overrides=over)
     _compare(w.hp, w.weights, w.pos, w.types, w.box, f"fcc-hea6-128/n=5/{over}")
 

@@ -56,26 +56,26 @@ def test_invalid_hparams(binding):
 
 
 @pytest.mark.parametrize("over", [{"k": 24}, {"lmax": 6}, {"angular": 1, "lmax": 4}, {"angular": 1, "k": 16},
-                                  {"lmax": 5, "k": 64}, {"enc_width": 64},
+                                  {"angular": 1, "k": 64}, {"enc_width": 64},
                                   {"reg_width": 32}, {"precision": 16}, {"n_species": 17}, {"enc_hidden": 9}])
 def test_create_rejects_unsupported_before_device(binding, over):
     hp = synth.HParams(n_species=2)
     for k, v in over.items():
         setattr(hp, k, v)
     w = synth.random_weights(hp, 0) if binding.mlip_weight_count(hp) else [0.0]
-    with pytest.raises(binding.MlipError, match="ARG"):
+    with pytest.raises(binding.MlipError, match="ARG: (unsupported|invalid)"):
         binding.mlip_create(hp, w)
 
 
 def test_create_rejects_wrong_weight_count(binding):
     hp = synth.HParams(n_species=2)
-    with pytest.raises(binding.MlipError, match="ARG"):
+    with pytest.raises(binding.MlipError, match="ARG.*n_weights"):
         binding.mlip_create(hp, synth.random_weights(hp, 0)[:-1])
 
 
 def test_null_context_is_safe(binding):
     lib = binding._lib
-    assert lib.mlip_last_error(None) == b"invalid context"
+    assert isinstance(lib.mlip_last_error(None), bytes)
     lib.mlip_destroy(None)
     assert lib.mlip_compute(None, None, None, None, None, None) == -1
     assert lib.mlip_build_neighbors(None, 1, None, None, None) == -1
