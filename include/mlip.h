@@ -168,6 +168,34 @@ mlip_status mlip_compute(mlip_ctx* ctx, const double* pos_dev, double* energy_de
                          double* forces_dev, double* virial_dev, double* totals_host);
 
 /*
+ * mlip_compute without device allocation, for callers that cannot allocate:
+ * code under HIP graph capture, tight serving loops, hosts that forbid
+ * hipMalloc after set-up.  Same arguments, evaluation and outputs as
+ * mlip_compute in the single-kernel configurations (MLIP_FUSION_CACHED,
+ * MLIP_FUSION_RECOMPUTE).  The fused kernel's per-work-group workspace, the
+ * block totals and the active-pair counter go to a fixed scratch array of
+ * MLIP_STATIC_SCRATCH_BYTES built into the library, one per device, which
+ * that device holds from the first call on it until the process ends; no
+ * allocating routine is called.
+ *
+ * Every call on one device shares that device's scratch and leaves its
+ * contents there (the totals and the counter are cleared at the start of a
+ * call, the workspace is written before it is read): calls that overlap on
+ * one device, from any context or stream, race and give wrong results.
+ * Serialise them.  The context's device must be current.
+ *
+ * Errors: those of mlip_compute; MLIP_E_ARG when the configuration is
+ * MLIP_FUSION_PARTIAL or MLIP_FUSION_UNFUSED (they keep per-atom
+ * intermediates the library allocates) or when the workspace of the current
+ * neighbour list (resident work-groups x per-work-group slot) exceeds the
+ * scratch (mlip_last_error gives both sizes); MLIP_E_HIP when the scratch
+ * cannot be resolved on the current device.
+ */
+#define MLIP_STATIC_SCRATCH_BYTES (256u * 1024u * 1024u)
+mlip_status mlip_compute_noalloc(mlip_ctx* ctx, const double* pos_dev, double* energy_dev,
+                                 double* forces_dev, double* virial_dev, double* totals_host);
+
+/*
  * Copy the neighbour list to the host in caller order: offsets_host int64
  * [n+1], idx_host int32 [offsets[n]] (use mlip_get_stats().n_listed_pairs to
  * size it).  Entries of a row are grouped by neighbour species.  Synchronises.

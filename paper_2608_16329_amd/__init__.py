@@ -54,6 +54,15 @@ class Potential:
         return binding.mlip_compute(self.ctx, pos.data_ptr(), energy.data_ptr() if energy is not None else None,
                                     forces.data_ptr(), virial.data_ptr() if virial is not None else None, totals)
 
+    def compute_noalloc(self, pos, forces, energy=None, virial=None, totals: bool = False) -> Optional[np.ndarray]:
+        """compute() with the library's fixed per-device scratch instead of
+        context buffers (mlip_compute_noalloc: no device allocation)."""
+        assert pos.is_cuda and pos.dtype == self.torch.float64 and pos.is_contiguous()
+        assert forces.is_cuda and forces.dtype == self.torch.float64 and forces.is_contiguous()
+        return binding.mlip_compute_noalloc(self.ctx, pos.data_ptr(),
+                                            energy.data_ptr() if energy is not None else None, forces.data_ptr(),
+                                            virial.data_ptr() if virial is not None else None, totals)
+
     def set_fusion(self, fusion: int) -> None:
         """binding.MLIP_FUSION_CACHED (default), _RECOMPUTE, _PARTIAL or _UNFUSED."""
         binding.mlip_set_fusion(self.ctx, fusion)

@@ -25,7 +25,9 @@ STATUS = {0: "MLIP_OK", -1: "MLIP_E_ARG", -2: "MLIP_E_OOM", -3: "MLIP_E_HIP", -4
 EXPORTED = ["mlip_weight_count", "mlip_create", "mlip_build_neighbors", "mlip_compute", "mlip_get_neighbors",
             "mlip_memory_bytes", "mlip_get_stats", "mlip_last_error", "mlip_destroy", "mlip_md_set_masses",
             "mlip_md_first_half", "mlip_md_second_half", "mlip_md_kinetic", "mlip_set_fusion",
-            "mlip_get_neighbor_rows"]
+            "mlip_get_neighbor_rows", "mlip_compute_noalloc"]
+
+MLIP_STATIC_SCRATCH_BYTES = 256 * 1024 * 1024
 
 MLIP_FUSION_CACHED, MLIP_FUSION_RECOMPUTE, MLIP_FUSION_PARTIAL, MLIP_FUSION_UNFUSED = 0, 1, 2, 3
 
@@ -67,6 +69,7 @@ def _load() -> ctypes.CDLL:
         "mlip_create": (st, [ctypes.POINTER(mlip_hparams), dp, ctypes.c_size_t, vp, ctypes.POINTER(vp)]),
         "mlip_build_neighbors": (st, [vp, ctypes.c_int64, vp, vp, dp]),
         "mlip_compute": (st, [vp, vp, vp, vp, vp, dp]),
+        "mlip_compute_noalloc": (st, [vp, vp, vp, vp, vp, dp]),
         "mlip_get_neighbors": (st, [vp, ip64, ip32]),
         "mlip_get_neighbor_rows": (st, [vp, ip64, ctypes.c_int64, ip64, ip32, ctypes.c_int64]),
         "mlip_memory_bytes": (st, [vp, ctypes.POINTER(ctypes.c_size_t)]),
@@ -130,6 +133,14 @@ def mlip_compute(ctx: int, pos_ptr: int, energy_ptr: Optional[int], forces_ptr: 
                  want_totals: bool = False) -> Optional[np.ndarray]:
     tot = np.zeros(10) if want_totals else None
     _check(ctx, _lib.mlip_compute(ctx, pos_ptr, energy_ptr or None, forces_ptr, virial_ptr or None, _dp(tot)))
+    return tot
+
+
+def mlip_compute_noalloc(ctx: int, pos_ptr: int, energy_ptr: Optional[int], forces_ptr: int,
+                         virial_ptr: Optional[int], want_totals: bool = False) -> Optional[np.ndarray]:
+    tot = np.zeros(10) if want_totals else None
+    _check(ctx, _lib.mlip_compute_noalloc(ctx, pos_ptr, energy_ptr or None, forces_ptr, virial_ptr or None,
+                                          _dp(tot)))
     return tot
 
 

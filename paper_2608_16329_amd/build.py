@@ -18,7 +18,7 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libmlip.so")
-SOURCES = ["api.cpp", "angular_tables.cpp", "neighbors.hip", "fused.hip", "unfused.hip", "md.hip"]
+SOURCES = ["api.cpp", "angular_tables.cpp", "neighbors.hip", "fused.hip", "unfused.hip", "md.hip", "scratch.hip"]
 ARCH = "gfx950"
 
 

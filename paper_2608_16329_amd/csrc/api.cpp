@@ -152,13 +152,22 @@ std::vector<double> transpose(const double* M, int rows, int cols) {
 }
 
 // Copy the totals to the host when asked (synchronising the stream).
-mlip_status finish_compute(mlip_ctx* ctx, double* totals_host) {
+mlip_status finish_compute(mlip_ctx* ctx, const double* d_totals, double* totals_host) {
   if (totals_host) {
-    MLIP_HIP(ctx, hipMemcpyAsync(totals_host, ctx->d_totals, 10 * sizeof(double), hipMemcpyDeviceToHost, ctx->stream));
+    MLIP_HIP(ctx, hipMemcpyAsync(totals_host, d_totals, 10 * sizeof(double), hipMemcpyDeviceToHost, ctx->stream));
     MLIP_HIP(ctx, hipStreamSynchronize(ctx->stream));
   }
   return MLIP_OK;
 }
+
+// Where one evaluation keeps its block totals, active-pair counter and
+// fused-kernel workspace: the context's buffers (mlip_compute) or the fixed
+// device scratch (mlip_compute_noalloc).
+struct ComputeScratch {
+  double* totals;                 // [16]
+  unsigned long long* counters;   // [4]
+  unsigned char* ws;              // ws_slot x n_blocks values
+};
 
 // The unfused configuration: ten kernels, one per equation, with the
 // per-entry and per-atom intermediates carved out of one device buffer
@@ -199,7 +208,7 @@ mlip_status compute_unfused(mlip_ctx* ctx, FusedArgs& a) {
   u.G = ctx->d_gbuf;
   u.forces = a.forces;
   u.virial = a.virial;
-  u.totals = ctx->d_totals;
+  u.totals = a.totals;
   for (int d = 0; d < 3; ++d) {
     u.box[d] = a.box[d];
     u.inv_box[d] = a.inv_box[d];
@@ -224,6 +233,84 @@ mlip_status compute_unfused(mlip_ctx* ctx, FusedArgs& a) {
   MLIP_HIP(ctx, launch_unfused(kUnfV, prec, u, s));                             // Eq. 9
   MLIP_HIP(ctx, launch_unfused(kUnfForce, prec, u, s));                         // Eq. 10
   return MLIP_OK;
+}
+
+// One evaluation (mlip_compute and mlip_compute_noalloc) with the given
+// scratch.  Allocates only in the three-kernel and unfused configurations.
+mlip_status run_compute(mlip_ctx* ctx, const double* pos_dev, double* energy_dev, double* forces_dev,
+                        double* virial_dev, double* totals_host, const ComputeScratch& sc) {
+  hipStream_t s = ctx->stream;
+  const int64_t n = ctx->n;
+  if (n == 0) {
+    if (totals_host)
+      for (int k = 0; k < 10; ++k) totals_host[k] = 0.0;
+    return MLIP_OK;
+  }
+  if (!pos_dev || !forces_dev) return fail(ctx, MLIP_E_ARG, "NULL positions or forces");
+  MLIP_HIP(ctx, launch_fill_f64(forces_dev, 3 * n, 0.0, s));
+  MLIP_HIP(ctx, launch_fill_f64(sc.totals, 16, 0.0, s));
+  MLIP_HIP(ctx, launch_fill_u64(sc.counters, 4, s));
+
+  FusedArgs a{};
+  a.pos = pos_dev;
+  a.types = ctx->d_types;
+  a.perm = ctx->d_perm;
+  a.offsets = ctx->d_offsets;
+  a.idx = ctx->d_idx;
+  a.enc = ctx->d_enc;
+  a.head = ctx->d_head;
+  a.qc = ctx->d_qc;
+  for (int l = 0; l < 8; ++l) a.lrow[l] = ctx->lrow[l];
+  a.energy = energy_dev;
+  a.forces = forces_dev;
+  a.virial = virial_dev;
+  a.totals = sc.totals;
+  a.counters = sc.counters;
+  a.ws = sc.ws;
+  a.ws_slot = (long long)ctx->ws_slot;
+  for (int d = 0; d < 3; ++d) {
+    a.box[d] = ctx->box[d];
+    a.inv_box[d] = 1.0 / ctx->box[d];
+  }
+  a.rc = ctx->hp.cutoff;
+  a.rc2 = ctx->hp.cutoff * ctx->hp.cutoff;
+  a.pi_rc = M_PI / ctx->hp.cutoff;
+  a.enc_stride = (long long)ctx->enc_stride;
+  a.head_stride = (long long)ctx->head_stride;
+  a.C = ctx->hp.n_species;
+  a.enc_cond = ctx->hp.enc_cond;
+  a.reg_cond = ctx->hp.reg_cond;
+  a.lmax = ctx->hp.lmax;
+  a.enc_hidden = ctx->hp.enc_hidden;
+  a.reg_hidden = ctx->hp.reg_hidden;
+  a.tile_atoms = ctx->tile_atoms;
+  a.n_tiles = int(ctx->n_tiles);
+  int t = 0;
+  for (int sp_i = 0; sp_i <= a.C; ++sp_i) {
+    a.species_start[sp_i] = ctx->species_start[sp_i];
+    a.tile_start[sp_i] = t;
+    if (sp_i < a.C) t += (ctx->species_start[sp_i + 1] - ctx->species_start[sp_i] + ctx->tile_atoms - 1) / ctx->tile_atoms;
+  }
+  if (ctx->fusion == MLIP_FUSION_PARTIAL || ctx->fusion == MLIP_FUSION_UNFUSED) {
+    const size_t need = size_t(n) * size_t((ctx->hp.lmax + 1) * ctx->hp.k) * ctx->elem_bytes;
+    MLIP_TRY(ensure(ctx, &ctx->d_gbuf, &ctx->cap_gbuf, need, "descriptor buffer"));
+    a.gbuf = ctx->d_gbuf;
+  }
+  if (ctx->fusion == MLIP_FUSION_UNFUSED && ctx->n_tiles > 0) {
+    MLIP_TRY(compute_unfused(ctx, a));
+    return finish_compute(ctx, sc.totals, totals_host);
+  }
+  if (ctx->n_tiles > 0) {
+    const int k = ctx->hp.k, prec = ctx->hp.precision;
+    if (ctx->fusion == MLIP_FUSION_PARTIAL) {
+      MLIP_HIP(ctx, launch_fused(k, prec, ctx->acfg, 2, a, ctx->n_blocks, s));
+      MLIP_HIP(ctx, launch_fused(k, prec, ctx->acfg, 3, a, ctx->n_blocks, s));
+      MLIP_HIP(ctx, launch_fused(k, prec, ctx->acfg, 4, a, ctx->n_blocks, s));
+    } else {
+      MLIP_HIP(ctx, launch_fused(k, prec, ctx->acfg, ctx->fusion == MLIP_FUSION_RECOMPUTE ? 1 : 0, a, ctx->n_blocks, s));
+    }
+  }
+  return finish_compute(ctx, sc.totals, totals_host);
 }
 
 }  // namespace
@@ -476,78 +563,42 @@ mlip_status mlip_compute(mlip_ctx* ctx, const double* pos_dev, double* energy_de
   if (!ctx) return MLIP_E_ARG;
   ctx->err.clear();
   if (!ctx->built) return fail(ctx, MLIP_E_STATE, "mlip_build_neighbors has not been called");
-  hipStream_t s = ctx->stream;
-  const int64_t n = ctx->n;
-  if (n == 0) {
-    if (totals_host)
-      for (int k = 0; k < 10; ++k) totals_host[k] = 0.0;
-    return MLIP_OK;
-  }
-  if (!pos_dev || !forces_dev) return fail(ctx, MLIP_E_ARG, "NULL positions or forces");
-  MLIP_HIP(ctx, launch_fill_f64(forces_dev, 3 * n, 0.0, s));
-  MLIP_HIP(ctx, launch_fill_f64(ctx->d_totals, 16, 0.0, s));
-  MLIP_HIP(ctx, launch_fill_u64(ctx->d_counters, 4, s));
+  const ComputeScratch sc{ctx->d_totals, ctx->d_counters, ctx->d_ws};
+  return run_compute(ctx, pos_dev, energy_dev, forces_dev, virial_dev, totals_host, sc);
+}
 
-  FusedArgs a{};
-  a.pos = pos_dev;
-  a.types = ctx->d_types;
-  a.perm = ctx->d_perm;
-  a.offsets = ctx->d_offsets;
-  a.idx = ctx->d_idx;
-  a.enc = ctx->d_enc;
-  a.head = ctx->d_head;
-  a.qc = ctx->d_qc;
-  for (int l = 0; l < 8; ++l) a.lrow[l] = ctx->lrow[l];
-  a.energy = energy_dev;
-  a.forces = forces_dev;
-  a.virial = virial_dev;
-  a.totals = ctx->d_totals;
-  a.counters = ctx->d_counters;
-  a.ws = ctx->d_ws;
-  a.ws_slot = (long long)ctx->ws_slot;
-  for (int d = 0; d < 3; ++d) {
-    a.box[d] = ctx->box[d];
-    a.inv_box[d] = 1.0 / ctx->box[d];
-  }
-  a.rc = ctx->hp.cutoff;
-  a.rc2 = ctx->hp.cutoff * ctx->hp.cutoff;
-  a.pi_rc = M_PI / ctx->hp.cutoff;
-  a.enc_stride = (long long)ctx->enc_stride;
-  a.head_stride = (long long)ctx->head_stride;
-  a.C = ctx->hp.n_species;
-  a.enc_cond = ctx->hp.enc_cond;
-  a.reg_cond = ctx->hp.reg_cond;
-  a.lmax = ctx->hp.lmax;
-  a.enc_hidden = ctx->hp.enc_hidden;
-  a.reg_hidden = ctx->hp.reg_hidden;
-  a.tile_atoms = ctx->tile_atoms;
-  a.n_tiles = int(ctx->n_tiles);
-  int t = 0;
-  for (int sp_i = 0; sp_i <= a.C; ++sp_i) {
-    a.species_start[sp_i] = ctx->species_start[sp_i];
-    a.tile_start[sp_i] = t;
-    if (sp_i < a.C) t += (ctx->species_start[sp_i + 1] - ctx->species_start[sp_i] + ctx->tile_atoms - 1) / ctx->tile_atoms;
-  }
-  if (ctx->fusion == MLIP_FUSION_PARTIAL || ctx->fusion == MLIP_FUSION_UNFUSED) {
-    const size_t need = size_t(n) * size_t((ctx->hp.lmax + 1) * ctx->hp.k) * ctx->elem_bytes;
-    MLIP_TRY(ensure(ctx, &ctx->d_gbuf, &ctx->cap_gbuf, need, "descriptor buffer"));
-    a.gbuf = ctx->d_gbuf;
-  }
-  if (ctx->fusion == MLIP_FUSION_UNFUSED && ctx->n_tiles > 0) {
-    MLIP_TRY(compute_unfused(ctx, a));
-    return finish_compute(ctx, totals_host);
-  }
-  if (ctx->n_tiles > 0) {
-    const int k = ctx->hp.k, prec = ctx->hp.precision;
-    if (ctx->fusion == MLIP_FUSION_PARTIAL) {
-      MLIP_HIP(ctx, launch_fused(k, prec, ctx->acfg, 2, a, ctx->n_blocks, s));
-      MLIP_HIP(ctx, launch_fused(k, prec, ctx->acfg, 3, a, ctx->n_blocks, s));
-      MLIP_HIP(ctx, launch_fused(k, prec, ctx->acfg, 4, a, ctx->n_blocks, s));
-    } else {
-      MLIP_HIP(ctx, launch_fused(k, prec, ctx->acfg, ctx->fusion == MLIP_FUSION_RECOMPUTE ? 1 : 0, a, ctx->n_blocks, s));
-    }
-  }
-  return finish_compute(ctx, totals_host);
+mlip_status mlip_compute_noalloc(mlip_ctx* ctx, const double* pos_dev, double* energy_dev, double* forces_dev,
+                                 double* virial_dev, double* totals_host) {
+  if (!ctx) return MLIP_E_ARG;
+  ctx->err.clear();
+  if (!ctx->built) return fail(ctx, MLIP_E_STATE, "mlip_build_neighbors has not been called");
+  if (ctx->fusion != MLIP_FUSION_CACHED && ctx->fusion != MLIP_FUSION_RECOMPUTE)
+    return fail(ctx, MLIP_E_ARG,
+                "mlip_compute_noalloc runs the single-kernel configurations only (cached or recompute); the "
+                "three-kernel and unfused ones hold per-atom intermediates the library allocates");
+  // workspace of the current list: one slot per resident work-group (none
+  // when the encoder output is recomputed)
+  const size_t ws_bytes =
+      ctx->fusion == MLIP_FUSION_CACHED ? ctx->ws_slot * size_t(ctx->n_blocks) * ctx->elem_bytes : 0;
+  if (kStaticScratchHeader + ws_bytes > kStaticScratchBytes)
+    return fail(ctx, MLIP_E_ARG,
+                "the fused kernel's workspace needs " + std::to_string(ws_bytes) + " bytes (" +
+                    std::to_string(ctx->n_blocks) + " work-groups x " +
+                    std::to_string(ctx->ws_slot * ctx->elem_bytes) + "); the fixed scratch holds " +
+                    std::to_string(kStaticScratchBytes - kStaticScratchHeader));
+  void* base = nullptr;
+  const hipError_t e = static_scratch_address(ctx->device, &base);
+  if (e != hipSuccess)
+    return fail_hip(ctx, e, "static scratch address (the context's device must be current)");
+  unsigned char* b = static_cast<unsigned char*>(base);
+  const ComputeScratch sc{reinterpret_cast<double*>(b), reinterpret_cast<unsigned long long*>(b + 128),
+                          b + kStaticScratchHeader};
+  MLIP_TRY(run_compute(ctx, pos_dev, energy_dev, forces_dev, virial_dev, totals_host, sc));
+  // the context's own counter keeps the active-pair count for mlip_get_stats
+  if (ctx->n > 0)
+    MLIP_HIP(ctx, hipMemcpyAsync(ctx->d_counters, sc.counters, sizeof(unsigned long long), hipMemcpyDeviceToDevice,
+                                 ctx->stream));
+  return MLIP_OK;
 }
 
 mlip_status mlip_get_neighbors(mlip_ctx* ctx, int64_t* offsets_host, int32_t* idx_host) {

@@ -26,6 +26,11 @@ constexpr int kHeadWidth = 64;            // head hidden width on the GPU path
 constexpr int kMaxHidden = 8;             // hidden layers supported on the GPU path
 constexpr int kAngRows = 16;              // angular rows, (lmax+1)^2 <= 16
 constexpr int kMonomials = 20;            // Cartesian monomials of degree <= 3
+// Fixed per-device scratch of mlip_compute_noalloc (MLIP_STATIC_SCRATCH_BYTES):
+// block totals and counters in the first 256 bytes, the fused kernel's
+// workspace after them.
+constexpr size_t kStaticScratchBytes = size_t(256) << 20;
+constexpr size_t kStaticScratchHeader = 256;
 
 // Number of values in one packed encoder table (device layout).
 inline size_t enc_table_elems(int k, int enc_hidden) {
@@ -233,6 +238,10 @@ constexpr int kModeRadial = 5;    // Eq. 2: distances -> g_rad, dg_rad/dr per en
 // order; k = 32, irreducible basis with l_max <= 3.
 enum UnfusedStage { kUnfSetup, kUnfAngular, kUnfMoment, kUnfDescriptor, kUnfAdjoint, kUnfU, kUnfV, kUnfForce };
 hipError_t launch_unfused(int stage, int precision, const UnfusedArgs& a, hipStream_t s);
+
+// scratch.hip: the device address of the fixed scratch on `device`, which
+// must be the current device; resolved on first use and kept per device.
+hipError_t static_scratch_address(int device, void** out);
 
 // md.hip
 hipError_t launch_md_first_half(double* pos, double* vel, const double* forces, const int32_t* types,
