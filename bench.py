@@ -31,8 +31,8 @@ PEAK_HBM_GBS = 8000.0
 FUSED_SOURCE = os.path.join(ROOT, "paper_2608_16329_amd", "csrc", "fused.hip")
 
 
-def traffic_summary_path(precision: int) -> str:
-    tag = "" if precision == 64 else "_f32"
+def traffic_summary_path(precision: int, fusion: str = "cached") -> str:
+    tag = ("" if precision == 64 else "_f32") + ("" if fusion == "cached" else "_" + fusion)
     return os.path.join(ROOT, "profiles", f"k_fused{tag}_fcc-hea6-128_traffic.md")
 
 
@@ -42,18 +42,19 @@ def fused_source_hash() -> str:
         return hashlib.sha256(f.read()).hexdigest()
 
 
-def measured_traffic(workload: str, n_atoms: int, precision: int):
+def measured_traffic(workload: str, n_atoms: int, precision: int, fusion: str = "cached"):
     """HBM bytes per launch of the fused kernel from the committed rocprofv3
     FETCH_SIZE / WRITE_SIZE summary, scaled by the same counters on a plain
     copy of known size; None when the summary is for other kernel source,
-    another workload or another precision."""
+    another workload, precision or fusion configuration."""
     try:
-        with open(traffic_summary_path(precision)) as f:
+        with open(traffic_summary_path(precision, fusion)) as f:
             for line in f:
                 if line.startswith("traffic_json:"):
                     t = json.loads(line.split(":", 1)[1])
                     if t["fused_source_sha256"] == fused_source_hash() and t["n_atoms"] == n_atoms \
-                            and t["workload"] == workload and t.get("precision", 64) == precision:
+                            and t["workload"] == workload and t.get("precision", 64) == precision \
+                            and t.get("fusion", "cached") == fusion:
                         return t["traffic_bytes_per_launch"]
     except (OSError, KeyError, ValueError):
         pass
@@ -111,14 +112,16 @@ def summarize_traffic(fetch_dir: str, write_dir: str, bench_log: str, copy_bytes
         if line.startswith("{"):
             b = json.loads(line)
     precision = b["config"].get("precision", 64)
+    fusion = b["config"].get("fusion", "cached")
     t = {"fused_source_sha256": fused_source_hash(), "workload": b["config"]["workload"],
-         "n_atoms": b["config"]["n_atoms"], "precision": precision, "fetch_kib_per_launch": float(np.mean(ff)),
+         "n_atoms": b["config"]["n_atoms"], "precision": precision, "fusion": fusion,
+         "fetch_kib_per_launch": float(np.mean(ff)),
          "write_kib_per_launch": float(np.mean(wf)), "copy_bytes": copy_bytes, "copy_fetch_kib": fc,
          "copy_write_kib": wc, "fetch_scale": f_scale, "write_scale": w_scale,
          "traffic_bytes_per_launch": fetch_b + write_b, "launches": len(ff)}
-    with open(traffic_summary_path(precision), "w") as f:
-        f.write(f"# HBM-side traffic of the fused energy/force/virial kernel (float{precision} network), "
-                "6-component FCC 128^3\n\n")
+    with open(traffic_summary_path(precision, fusion), "w") as f:
+        f.write(f"# HBM-side traffic of the fused energy/force/virial kernel (float{precision} network, "
+                f"{fusion} configuration), 6-component FCC 128^3\n\n")
         f.write("Two rocprofv3 counter runs of the same command (one counter per run), from the repository\n"
                 "root on the GPU host:\n\n")
         for ctr in ("FETCH_SIZE", "WRITE_SIZE"):
@@ -131,13 +134,19 @@ def summarize_traffic(fetch_dir: str, write_dir: str, bench_log: str, copy_bytes
                 f"{np.mean(wf):.4g} KiB; scaled traffic {fetch_b / 1e9:.1f} GB read + {write_b / 1e9:.1f} GB "
                 f"written = {(fetch_b + write_b) / 1e9:.1f} GB per launch "
                 f"({(fetch_b + write_b) / b['config']['n_atoms']:.0f} B per atom).\n\n")
-        ws = 2 * 2 * b["config"]["k"] * (precision // 8) * b["config"]["active_pairs_per_atom"]
-        f.write(f"Most of it is the per-pair (m, dm) workspace that pass 1 writes and pass 2 reads back: 2k values per "
-                f"active pair each way, {ws:.0f} B per atom at {b['config']['active_pairs_per_atom']:.2f} active pairs "
-                f"per atom; the per-work-group workspace (about a megabyte per tile) does not stay in the 4 MB L2 of an "
-                f"XCD between the two passes. The rest ({(fetch_b + write_b) / b['config']['n_atoms'] - ws:.0f} B per "
-                f"atom) is neighbour positions, neighbour-list entries, weights missing L2, and outputs. The counters "
-                f"see L2-to-fabric requests, which include Infinity Cache hits.\n\n")
+        if fusion == "cached":
+            ws = 2 * 2 * b["config"]["k"] * (precision // 8) * b["config"]["active_pairs_per_atom"]
+            f.write(f"Most of it is the per-pair (m, dm) workspace that pass 1 writes and pass 2 reads back: 2k values "
+                    f"per active pair each way, {ws:.0f} B per atom at {b['config']['active_pairs_per_atom']:.2f} active "
+                    f"pairs per atom; the per-work-group workspace (about a megabyte per tile) does not stay in the 4 MB "
+                    f"L2 of an XCD between the two passes. The rest "
+                    f"({(fetch_b + write_b) / b['config']['n_atoms'] - ws:.0f} B per atom) is neighbour positions, "
+                    f"neighbour-list entries, weights missing L2, and outputs. ")
+        else:
+            f.write("This configuration keeps no workspace: the traffic is neighbour positions, neighbour-list "
+                    "entries, encoder weights missing L2, and the outputs. ")
+        f.write("The counters see L2-to-fabric requests, which include Infinity Cache hits: no counter of this "
+                "part separates Infinity Cache hits from HBM accesses.\n\n")
         f.write("traffic_json: " + json.dumps(t) + "\n")
     print(json.dumps(t))
 
@@ -255,6 +264,36 @@ def capacity_sweep(edges, steps: int, seed: int, bpa: float = 450.0, precision: 
         del pos, vel, types, F
 
 
+def recompute_record(pot, pos, F, E, V, stream, evals: int, flop: float, N: int, w, precision: int) -> dict:
+    """The recompute configuration (one kernel, the encoder evaluated again in
+    pass 2 instead of parked in a workspace: nothing but the outputs goes to
+    HBM) at the final positions of the timed steps: HIP-event time of
+    `evals` evaluations after one untimed, the same algorithmic FLOP."""
+    import torch
+    pot.set_fusion(1)
+    lib_bytes = pot.memory_bytes()
+    pot.compute(pos, F, E, V)
+    ev = []
+    for _ in range(evals):
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        pot.compute(pos, F, E, V)
+        e1.record(stream)
+        ev.append((e0, e1))
+    torch.cuda.synchronize()
+    pot.set_fusion(0)
+    ms = float(np.mean([a.elapsed_time(b) for a, b in ev]))
+    achieved = flop / (ms * 1e-3) / 1e12
+    traffic = measured_traffic(w.description, N, precision, "recompute")
+    log(f"[bench] recompute configuration: {ms:.1f} ms per evaluation")
+    return {"fusion": "recompute", "evaluations": evals, "kernel_ms": ms, "atom_evals_per_s": N / (ms * 1e-3),
+            "achieved": achieved, "peak": PEAK_TFLOPS[precision], "unit": "TFLOP/s",
+            "frac": achieved / PEAK_TFLOPS[precision], "traffic": traffic,
+            "traffic_gbps": traffic / (ms * 1e-3) / 1e9 if traffic else None,
+            "library_bytes_per_atom": lib_bytes / N}
+
+
 def log(msg: str) -> None:
     print(msg, file=sys.stderr, flush=True)
 
@@ -292,8 +331,12 @@ def cpu_baseline(w, target_atoms: int) -> dict:
     lpos = d[loc] + reach + rl
     ltypes = w.types[loc]
     centres = np.nonzero(inner[loc])[0]
+    t_nbr = time.perf_counter()
     off, idx = cell_list_neighbors(lpos, lbox, rl)
-    cores = min(16, len(os.sched_getaffinity(0)))
+    t_nbr = time.perf_counter() - t_nbr
+    host_cores = len(os.sched_getaffinity(0))
+    # one GPU's share of a GPU host: at most 16 processes, whatever the host has
+    cores = min(16, host_cores)
     chunks = np.array_split(centres, cores)
     jobs = [(w.hp, w.weights, lpos, ltypes, lbox, off, idx, c) for c in chunks if len(c)]
     ctx = mp.get_context("fork")
@@ -301,11 +344,14 @@ def cpu_baseline(w, target_atoms: int) -> dict:
     with ctx.Pool(len(jobs)) as pool:
         pool.map(_oracle_worker, jobs)
     wall = time.perf_counter() - t0
-    return {"value": len(centres) / wall, "unit": "atom-steps/s", "cores": len(jobs), "kind": "oracle",
-            "cpu_model": host_cpu_model(),
+    return {"value": len(centres) / (wall + t_nbr), "unit": "atom-steps/s", "cores": len(jobs), "kind": "oracle",
+            "cpu_model": host_cpu_model(), "host_cores": host_cores,
+            "cores_cap": "16 processes, one GPU's share of the GPU host's cores",
+            "evaluation_only_value": len(centres) / wall,
             "sample": f"{len(centres)} centre atoms of the same workload (a cube at the box centre), "
                       f"one E+F+virial evaluation each, float64 NumPy, {len(jobs)} processes x 1 BLAS "
-                      f"thread, {wall:.1f} s wall; neighbour search not timed"}
+                      f"thread, {wall:.1f} s wall, plus the oracle's cell-list neighbour search of the "
+                      f"{len(lpos)}-atom region around it in one process, {t_nbr:.1f} s"}
 
 
 def host_cpu_model() -> str:
@@ -334,9 +380,15 @@ def main() -> int:
                     help="fusion configuration: one kernel caching the encoder output (default), one kernel "
                          "recomputing it, three kernels with the descriptor in HBM, or ten kernels (one per "
                          "equation) with every intermediate in HBM")
+    ap.add_argument("--scatter", choices=("atomic", "tile"), default="atomic",
+                    help="F_j scatter of the cached kernel: one atomic per pair (default) or summed per distinct "
+                         "neighbour of a tile in LDS first")
     ap.add_argument("--hp", default="",
                     help="comma-separated hyper-parameter overrides, e.g. k=64,lmax=2,enc_cond=1")
     ap.add_argument("--rebuild-every", type=int, default=10)
+    ap.add_argument("--recompute-evals", type=int, default=3,
+                    help="after the timed steps of the cached configuration, time this many evaluations of the "
+                         "recompute configuration (0 disables)")
     ap.add_argument("--cpu-sample", type=int, default=100000, help="oracle sample size (atoms); 0 disables")
     ap.add_argument("--calibrate-copy-bytes", type=int, default=0,
                     help="first run one device-to-device copy of this many bytes (counter calibration)")
@@ -353,8 +405,9 @@ def main() -> int:
         return 0
     if args.summarize_traffic:
         summarize_traffic(*args.summarize_traffic, copy_bytes=args.calibrate_copy_bytes or 2147483648,
-                          command="python3 <repo>/bench.py --steps 1 --warmup 0 --cpu-sample 0 "
-                                  f"--calibrate-copy-bytes 2147483648 --precision {args.precision}")
+                          command="python3 <repo>/bench.py --steps 1 --warmup 0 --cpu-sample 0 --recompute-evals 0 "
+                                  f"--calibrate-copy-bytes 2147483648 --precision {args.precision} "
+                                  f"--fusion {args.fusion}")
         return 0
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -396,6 +449,7 @@ def main() -> int:
     stream = torch.cuda.current_stream()
     pot = Potential(w.hp, w.weights, stream=stream)
     pot.set_fusion({"cached": 0, "recompute": 1, "partial": 2, "unfused": 3}[args.fusion])
+    pot.set_scatter({"atomic": 0, "tile": 1}[args.scatter])
     pot.set_masses(w.masses)
     t0 = time.perf_counter()
     pot.build_neighbors(pos, types, w.box)
@@ -464,7 +518,11 @@ def main() -> int:
     used = free0 - free1
     bpa = used / N
 
-    traffic = measured_traffic(w.description, N, args.precision) if args.fusion == "cached" else None
+    traffic = measured_traffic(w.description, N, args.precision, args.fusion) if args.scatter == "atomic" else None
+    recompute = None
+    if args.fusion == "cached" and args.recompute_evals > 0 and w.hp.k == 32 and w.hp.lmax <= 3 \
+            and w.hp.angular == 0:
+        recompute = recompute_record(pot, pos, F, E, V, stream, args.recompute_evals, flop, N, w, args.precision)
     result = {
         "metric": "atom-steps/s (E+F+virial) at 1 GPU",
         "value": value,
@@ -486,7 +544,7 @@ def main() -> int:
                    "listed_pairs_per_atom": st["n_listed_pairs"] / N, "tile_atoms": st["tile_atoms"],
                    "blocks": st["n_blocks"], "seed": args.seed, "precision": args.precision,
                    "enc_cond": w.hp.enc_cond, "reg_cond": w.hp.reg_cond, "enc_hidden": w.hp.enc_hidden,
-                   "reg_hidden": w.hp.reg_hidden, "fusion": args.fusion},
+                   "reg_hidden": w.hp.reg_hidden, "fusion": args.fusion, "scatter": args.scatter},
         "roofline": {"bound": "mfma", "achieved": achieved, "peak": PEAK_TFLOPS[args.precision], "unit": "TFLOP/s",
                      "frac": achieved / PEAK_TFLOPS[args.precision],
                      "traffic": traffic,
@@ -499,6 +557,7 @@ def main() -> int:
                      "kernel_ms": ms_compute,
                      "algorithmic_flop_per_launch": flop},
         "compute_only_atom_evals_per_s": N / (ms_median * 1e-3),
+        "recompute": recompute,
         "hbm_bytes_per_atom": bpa,
         "library_bytes_per_atom": lib_bytes / N,
         "caller_bytes_per_atom": caller_bytes / N,

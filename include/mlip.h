@@ -252,12 +252,32 @@ typedef enum {
 /*
  * Select the fusion configuration for later mlip_compute calls.  The
  * configurations other than MLIP_FUSION_CACHED exist for k = 32 with the
- * irreducible basis and l_max <= 3.  Synchronises the stream and releases
- * the buffers of a configuration that is left.
+ * irreducible basis and l_max <= 3.  Synchronises the stream, releases the
+ * buffers of a configuration that is left and, after a neighbour build,
+ * allocates the per-work-group workspace of the cached and three-kernel
+ * configurations (MLIP_E_OOM if it does not fit); the recompute and unfused
+ * configurations hold none.
  * Errors: MLIP_E_ARG (unknown value, or a non-default one with other
- * hyper-parameters), MLIP_E_HIP.
+ * hyper-parameters), MLIP_E_OOM, MLIP_E_HIP.
  */
 mlip_status mlip_set_fusion(mlip_ctx* ctx, int32_t fusion);
+
+/*
+ * How the cached single kernel adds -f_ij to F_j (Section 3.1: the forces are
+ * the scatter-sum of the partial forces), for measuring the two designs
+ * against each other; both give the same forces up to rounding order.
+ *   MLIP_SCATTER_ATOMIC  one float64 atomic add to HBM per pair and
+ *                        component (default)
+ *   MLIP_SCATTER_TILE    contributions summed per distinct neighbour of a
+ *                        tile in an LDS table, then one atomic add per
+ *                        neighbour and component
+ * Applies to MLIP_FUSION_CACHED at k = 32 with the irreducible basis and
+ * l_max <= 3 (the other configurations scatter by atomics).  Errors:
+ * MLIP_E_ARG (unknown value, or MLIP_SCATTER_TILE with other
+ * hyper-parameters).
+ */
+typedef enum { MLIP_SCATTER_ATOMIC = 0, MLIP_SCATTER_TILE = 1 } mlip_scatter;
+mlip_status mlip_set_scatter(mlip_ctx* ctx, int32_t scatter);
 
 /* Device memory held by the context, in bytes. */
 mlip_status mlip_memory_bytes(const mlip_ctx* ctx, size_t* bytes);

@@ -67,6 +67,10 @@ class Potential:
         """binding.MLIP_FUSION_CACHED (default), _RECOMPUTE, _PARTIAL or _UNFUSED."""
         binding.mlip_set_fusion(self.ctx, fusion)
 
+    def set_scatter(self, scatter: int) -> None:
+        """binding.MLIP_SCATTER_ATOMIC (default) or MLIP_SCATTER_TILE."""
+        binding.mlip_set_scatter(self.ctx, scatter)
+
     def neighbors(self):
         return binding.mlip_get_neighbors(self.ctx)
 

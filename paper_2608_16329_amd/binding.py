@@ -25,11 +25,12 @@ STATUS = {0: "MLIP_OK", -1: "MLIP_E_ARG", -2: "MLIP_E_OOM", -3: "MLIP_E_HIP", -4
 EXPORTED = ["mlip_weight_count", "mlip_create", "mlip_build_neighbors", "mlip_compute", "mlip_get_neighbors",
             "mlip_memory_bytes", "mlip_get_stats", "mlip_last_error", "mlip_destroy", "mlip_md_set_masses",
             "mlip_md_first_half", "mlip_md_second_half", "mlip_md_kinetic", "mlip_set_fusion",
-            "mlip_get_neighbor_rows", "mlip_compute_noalloc"]
+            "mlip_get_neighbor_rows", "mlip_compute_noalloc", "mlip_set_scatter"]
 
 MLIP_STATIC_SCRATCH_BYTES = 256 * 1024 * 1024
 
 MLIP_FUSION_CACHED, MLIP_FUSION_RECOMPUTE, MLIP_FUSION_PARTIAL, MLIP_FUSION_UNFUSED = 0, 1, 2, 3
+MLIP_SCATTER_ATOMIC, MLIP_SCATTER_TILE = 0, 1
 
 
 class mlip_hparams(ctypes.Structure):
@@ -81,6 +82,7 @@ def _load() -> ctypes.CDLL:
         "mlip_md_second_half": (st, [vp, vp, vp, ctypes.c_double]),
         "mlip_md_kinetic": (st, [vp, vp, dp]),
         "mlip_set_fusion": (st, [vp, ctypes.c_int32]),
+        "mlip_set_scatter": (st, [vp, ctypes.c_int32]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -173,6 +175,10 @@ def mlip_get_neighbor_rows(ctx: int, atoms, cap: int):
 
 def mlip_set_fusion(ctx: int, fusion: int) -> None:
     _check(ctx, _lib.mlip_set_fusion(ctx, int(fusion)))
+
+
+def mlip_set_scatter(ctx: int, scatter: int) -> None:
+    _check(ctx, _lib.mlip_set_scatter(ctx, int(scatter)))
 
 
 def mlip_memory_bytes(ctx: int) -> int:

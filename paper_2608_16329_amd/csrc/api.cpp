@@ -160,6 +160,17 @@ mlip_status finish_compute(mlip_ctx* ctx, const double* d_totals, double* totals
   return MLIP_OK;
 }
 
+// The fused kernel's per-work-group workspace, held only in the
+// configurations whose kernels park (m, dm) in it (cached, and the
+// derivation kernel of the three-kernel split); sized by the last build.
+mlip_status ensure_workspace(mlip_ctx* ctx) {
+  if (ctx->fusion == MLIP_FUSION_CACHED || ctx->fusion == MLIP_FUSION_PARTIAL)
+    return ensure(ctx, &ctx->d_ws, &ctx->cap_ws, ctx->ws_slot * size_t(ctx->n_blocks) * ctx->elem_bytes, "workspace");
+  release(ctx, &ctx->d_ws, ctx->cap_ws);
+  ctx->cap_ws = 0;
+  return MLIP_OK;
+}
+
 // Where one evaluation keeps its block totals, active-pair counter and
 // fused-kernel workspace: the context's buffers (mlip_compute) or the fixed
 // device scratch (mlip_compute_noalloc).
@@ -307,7 +318,9 @@ mlip_status run_compute(mlip_ctx* ctx, const double* pos_dev, double* energy_dev
       MLIP_HIP(ctx, launch_fused(k, prec, ctx->acfg, 3, a, ctx->n_blocks, s));
       MLIP_HIP(ctx, launch_fused(k, prec, ctx->acfg, 4, a, ctx->n_blocks, s));
     } else {
-      MLIP_HIP(ctx, launch_fused(k, prec, ctx->acfg, ctx->fusion == MLIP_FUSION_RECOMPUTE ? 1 : 0, a, ctx->n_blocks, s));
+      const int mode = ctx->fusion == MLIP_FUSION_RECOMPUTE ? 1
+                       : (ctx->scatter == MLIP_SCATTER_TILE ? kModeCachedTileFj : 0);
+      MLIP_HIP(ctx, launch_fused(k, prec, ctx->acfg, mode, a, ctx->n_blocks, s));
     }
   }
   return finish_compute(ctx, sc.totals, totals_host);
@@ -551,8 +564,7 @@ mlip_status mlip_build_neighbors(mlip_ctx* ctx, int64_t n_atoms, const double* p
   ctx->n_blocks = int(std::max<int64_t>(1, std::min<int64_t>(tiles, ctx->n_cu)));
   const int64_t chunks = std::min<int64_t>(tile_chunk_cap(tm), (int64_t(T) * ctx->max_row + 15) / 16 + C);
   ctx->ws_slot = size_t(chunks) * 2 * size_t(ctx->hp.k) * 16;
-  MLIP_TRY(ensure(ctx, &ctx->d_ws, &ctx->cap_ws, ctx->ws_slot * size_t(ctx->n_blocks) * ctx->elem_bytes,
-                  "workspace"));
+  MLIP_TRY(ensure_workspace(ctx));
   ctx->built = true;
   ctx->n_builds += 1;
   return MLIP_OK;
@@ -692,6 +704,21 @@ mlip_status mlip_set_fusion(mlip_ctx* ctx, int32_t fusion) {
     ctx->cap_gbuf = 0;
   }
   ctx->fusion = fusion;
+  // the workspace follows the configuration (sized by the last build)
+  if (ctx->built && ctx->n > 0) MLIP_TRY(ensure_workspace(ctx));
+  else if (fusion != MLIP_FUSION_CACHED && fusion != MLIP_FUSION_PARTIAL) MLIP_TRY(ensure_workspace(ctx));
+  return MLIP_OK;
+}
+
+mlip_status mlip_set_scatter(mlip_ctx* ctx, int32_t scatter) {
+  if (!ctx) return MLIP_E_ARG;
+  ctx->err.clear();
+  if (scatter != MLIP_SCATTER_ATOMIC && scatter != MLIP_SCATTER_TILE)
+    return fail(ctx, MLIP_E_ARG, "unknown scatter variant");
+  if (scatter == MLIP_SCATTER_TILE && (ctx->hp.k != 32 || ctx->acfg != 0))
+    return fail(ctx, MLIP_E_ARG, "the tile-reduced scatter exists for k = 32 and the irreducible basis with "
+                                 "l_max <= 3 only");
+  ctx->scatter = scatter;
   return MLIP_OK;
 }
 

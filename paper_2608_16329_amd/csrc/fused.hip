@@ -16,7 +16,9 @@
 //      moment P_i = sum_j g_ang (x) g_rad (Eq. 4) is another MFMA product
 //      (K = pairs), accumulated into LDS.  The pre-cutoff output m and its
 //      tangent dm (2k values per pair) go to a fixed-size per-work-group
-//      workspace; nothing is recomputed in pass 2.
+//      workspace; nothing is recomputed in pass 2.  When the encoder is
+//      recomputed in pass 2 instead (no workspace), pass 1 runs the forward
+//      products alone: the moment needs m only.
 //   C. Descriptor (Eq. 5), energy head (Eq. 6) and its gradient, and
 //      W_i = dE_i/dP_i (Eq. 7) for the tile's atoms, in LDS (W overwrites P).
 //   D. Pass 2, per chunk: v = W g and the reassociated radial term
@@ -240,6 +242,10 @@ __device__ __forceinline__ void monomials_n(R x, R y, R z, R m[NM], R gx[NM], R 
   }
 }
 
+// Slots of the per-tile table of the tile-reduced force scatter: a tile of
+// up to 32 atoms has a few hundred distinct neighbours.
+constexpr int kFjSlots = 1024;
+
 template <int K, int TM, typename R, int NW, int DR, int NM>
 struct Smem {
   R P[TM][DR][K + 1];  // moment, then its adjoint W (padded rows)
@@ -252,6 +258,12 @@ struct Smem {
       R yT[kHeadWidth][TM > 16 ? 32 : 16];             // head activations
       R gT[kHeadWidth][TM > 16 ? 32 : 16];             // head backward scratch
     } hd;
+    // pass 2 of the cached configuration with the tile-reduced force
+    // scatter: the tile's F_j contributions summed per neighbour j
+    struct {
+      int key[kFjSlots];        // neighbour index, -1 = empty
+      double val[kFjSlots][3];
+    } fj;
   } u;
   R qc[DR][NM];        // angular features over the monomials
   R rw[DR];            // descriptor weight of each angular row (metric C_l)
@@ -394,8 +406,11 @@ __device__ __forceinline__ const R* chunk_table(const FusedArgs& A, const Smem<K
 // from the LDS copy of (w0, b0), then the residual hidden layers Z = W H as
 // 8 x 32 MFMA steps whose forward and tangent columns share each weight
 // fragment.  On return h[T][i], dh[T][i] hold rows 16T + drow(i, g) of
-// column c; the result is the output-layer section of the table.
-template <int K, int TM, typename R, int NW, int DR, int NM>
+// column c; the result is the output-layer section of the table.  Without
+// kTan only the forward runs (dh is left untouched): the moment needs the
+// encoder output alone, so a pass 1 that keeps no workspace skips the
+// tangent's half of the products.
+template <int K, int TM, typename R, int NW, int DR, int NM, bool kTan = true>
 __device__ __forceinline__ const R* encoder_hidden(const FusedArgs& A, const Smem<K, TM, R, NW, DR, NM>& S, int sj, R r,
                                                    const R* __restrict__ tab, R (&h)[8][4], R (&dh)[8][4]) {
   typedef Stream<K, R> St;
@@ -410,7 +425,7 @@ __device__ __forceinline__ const R* encoder_hidden(const FusedArgs& A, const Sme
       const R w0 = S.u.l0[sj][0][in], z = w0 * r + S.u.l0[sj][1][in];
       const R s = sigmoid(z);
       h[T][i] = z * s;
-      dh[T][i] = s * (R(1) + z * (R(1) - s)) * w0;
+      if constexpr (kTan) dh[T][i] = s * (R(1) + z * (R(1) - s)) * w0;
     }
   const R* __restrict__ layer = tab + 2 * kEncWidth;
   for (int t = 1; t < A.enc_hidden; ++t) {
@@ -441,7 +456,7 @@ __device__ __forceinline__ const R* encoder_hidden(const FusedArgs& A, const Sme
       for (int To = 0; To < 8; ++To) {
         const R wv = wb[ks % kRing][To / VW][To % VW];
         acc[To] = mfma(wv, h[T][i], acc[To]);
-        dacc[To] = mfma(wv, dh[T][i], dacc[To]);
+        if constexpr (kTan) dacc[To] = mfma(wv, dh[T][i], dacc[To]);
       }
       __builtin_amdgcn_sched_barrier(0);
     }
@@ -453,18 +468,18 @@ __device__ __forceinline__ const R* encoder_hidden(const FusedArgs& A, const Sme
         const R z = acc[To][q];
         const R s = sigmoid(z);
         h[To][q] += z * s;
-        dh[To][q] += s * (R(1) + z * (R(1) - s)) * dacc[To][q];
+        if constexpr (kTan) dh[To][q] += s * (R(1) + z * (R(1) - s)) * dacc[To][q];
       }
   }
   return layer;
 }
 
 // Encoder output layer with pairs as rows: mo[Tc] register q holds
-// m[pair drow(q, g)][16Tc + c] (dmo the same for the tangent).  Even and odd
-// k-steps accumulate separately so 4 KT independent MFMA chains are in
-// flight; the bias is added at the end so the first products do not wait
-// for its load.
-template <int K, typename R>
+// m[pair drow(q, g)][16Tc + c] (dmo the same for the tangent, computed only
+// with kTan).  Even and odd k-steps accumulate separately so 4 KT independent
+// MFMA chains are in flight; the bias is added at the end so the first
+// products do not wait for its load.
+template <int K, typename R, bool kTan = true>
 __device__ __forceinline__ void encoder_out_rows(const R* __restrict__ layer, const R (&h)[8][4], const R (&dh)[8][4],
                                                  v4<R> (&mo)[K / 16], v4<R> (&dmo)[K / 16]) {
   typedef Stream<K, R> St;
@@ -497,14 +512,14 @@ __device__ __forceinline__ void encoder_out_rows(const R* __restrict__ layer, co
     for (int Tc = 0; Tc < KT; ++Tc) {
       const R wv = wo[ks % kRing][Tc / VO][Tc % VO];
       mo2[ks & 1][Tc] = mfma(h[T][i], wv, mo2[ks & 1][Tc]);
-      dmo2[ks & 1][Tc] = mfma(dh[T][i], wv, dmo2[ks & 1][Tc]);
+      if constexpr (kTan) dmo2[ks & 1][Tc] = mfma(dh[T][i], wv, dmo2[ks & 1][Tc]);
     }
     __builtin_amdgcn_sched_barrier(0);
   }
 #pragma unroll
   for (int Tc = 0; Tc < KT; ++Tc) {
     mo[Tc] = mo2[0][Tc] + mo2[1][Tc] + v4<R>{b[Tc], b[Tc], b[Tc], b[Tc]};
-    dmo[Tc] = dmo2[0][Tc] + dmo2[1][Tc];
+    if constexpr (kTan) dmo[Tc] = dmo2[0][Tc] + dmo2[1][Tc];
   }
 }
 
@@ -558,8 +573,8 @@ __device__ __forceinline__ void encoder_out_cols(const R* __restrict__ layer, co
     }
 }
 
-// Pass 1 on one chunk: encoder forward + tangent, moment accumulation and,
-// when kWs, the workspace write of (m, dm).
+// Pass 1 on one chunk: encoder forward, moment accumulation and, when kWs,
+// the encoder tangent and the workspace write of (m, dm).
 template <int K, int TM, typename R, int NW, int DR, int NM, bool kWs>
 __device__ void pass1_chunk(const FusedArgs& A, Smem<K, TM, R, NW, DR, NM>& S, int ch, const PairPos pp, R* __restrict__ wsc) {
   constexpr int KT = K / 16;
@@ -580,9 +595,10 @@ __device__ void pass1_chunk(const FusedArgs& A, Smem<K, TM, R, NW, DR, NM>& S, i
   if (atom < 0) fc = R(0);
 
   R h[8][4], dh[8][4];
-  const R* __restrict__ layer = encoder_hidden(A, S, S.ch_s[ch], r, chunk_table(A, S, ch), h, dh);
+  const R* __restrict__ layer =
+      encoder_hidden<K, TM, R, NW, DR, NM, kWs>(A, S, S.ch_s[ch], r, chunk_table(A, S, ch), h, dh);
   v4<R> mo[KT], dmo[KT];
-  encoder_out_rows<K, R>(layer, h, dh, mo, dmo);
+  encoder_out_rows<K, R, kWs>(layer, h, dh, mo, dmo);
 
   // moment: P[mm][col] += sum_pairs fc * a_mm(u) * m[pair][col], one MFMA
   // product per centre atom present in the chunk and 16-row tile of the
@@ -695,8 +711,32 @@ __device__ __forceinline__ void pass2_recompute(const FusedArgs& A, const Smem<K
   in.pp = pp;
 }
 
-// Pass 2 on one chunk: W contractions, partial forces and scatter.
+// F_j -= f_ij through the tile's table in LDS (open addressing by a
+// multiplicative hash of j, linear probing); when every probe position of j
+// is taken by other neighbours the contribution goes straight to HBM.
 template <int K, int TM, typename R, int NW, int DR, int NM>
+__device__ __forceinline__ void scatter_fj_tile(const FusedArgs& A, Smem<K, TM, R, NW, DR, NM>& S, int j, double fx,
+                                                double fy, double fz) {
+  constexpr int kProbes = 32;
+  int slot = int((unsigned(j) * 0x9E3779B1u) >> 22);  // 10 bits: kFjSlots = 1024
+  for (int p = 0; p < kProbes; ++p) {
+    const int prev = atomicCAS(&S.u.fj.key[slot], -1, j);
+    if (prev == -1 || prev == j) {
+      atomicAdd(&S.u.fj.val[slot][0], -fx);
+      atomicAdd(&S.u.fj.val[slot][1], -fy);
+      atomicAdd(&S.u.fj.val[slot][2], -fz);
+      return;
+    }
+    slot = (slot + 1) & (kFjSlots - 1);
+  }
+  atomicAdd(&A.forces[3 * (long long)j], -fx);
+  atomicAdd(&A.forces[3 * (long long)j + 1], -fy);
+  atomicAdd(&A.forces[3 * (long long)j + 2], -fz);
+}
+
+// Pass 2 on one chunk: W contractions, partial forces and scatter (F_j by
+// global atomics, or with kTileFj through the tile's table).
+template <int K, int TM, typename R, int NW, int DR, int NM, bool kTileFj = false>
 __device__ void pass2_chunk(const FusedArgs& A, Smem<K, TM, R, NW, DR, NM>& S, int ch, const Pass2In<K, R>& in) {
   constexpr int KT = K / 16;
   const int lane = threadIdx.x & 63, g = lane >> 4, c = lane & 15;
@@ -798,9 +838,13 @@ __device__ void pass2_chunk(const FusedArgs& A, Smem<K, TM, R, NW, DR, NM>& S, i
   const double fz = double(s * uz + (tz - ut * uz) * ir);
   if (valid) {
     if (g == 0) {
-      atomicAdd(&A.forces[3 * (long long)j], -fx);
-      atomicAdd(&A.forces[3 * (long long)j + 1], -fy);
-      atomicAdd(&A.forces[3 * (long long)j + 2], -fz);
+      if constexpr (kTileFj) {
+        scatter_fj_tile(A, S, j, fx, fy, fz);
+      } else {
+        atomicAdd(&A.forces[3 * (long long)j], -fx);
+        atomicAdd(&A.forces[3 * (long long)j + 1], -fy);
+        atomicAdd(&A.forces[3 * (long long)j + 2], -fz);
+      }
     } else if (g == 1) {
       atomicAdd(&S.Fi[atom][0], fx);
       atomicAdd(&S.Fi[atom][1], fy);
@@ -1151,7 +1195,8 @@ __device__ __forceinline__ void stage_first_layer(const FusedArgs& A, Smem<K, TM
 // (Eqs. 1-5, G to HBM), regression (Eq. 6, E and dE/dG to HBM) and
 // derivation (Eqs. 7-10, recomputing P); or the radial kernel of the unfused
 // configuration (Eq. 2 alone, which uses the regression kernel as well).
-enum Mode { kCached = 0, kRecompute = 1, kEncode = 2, kRegress = 3, kDerive = 4, kRadial = 5 };
+enum Mode { kCached = 0, kRecompute = 1, kEncode = 2, kRegress = 3, kDerive = 4, kRadial = 5, kCachedTileFj = 6 };
+static_assert(kCachedTileFj == kModeCachedTileFj, "mode number of the tile-reduced scatter");
 static_assert(kRegress == kModeRegress && kRadial == kModeRadial, "mode numbers of the unfused configuration");
 
 template <int K, int TM, typename R, int NW, int DR, int NM, int MODE>
@@ -1347,7 +1392,7 @@ __global__ __launch_bounds__(64 * NW, 1) void k_fused(FusedArgs A) {
       __syncthreads();
       continue;
     } else {
-      constexpr bool kWs = MODE == kCached || MODE == kDerive;
+      constexpr bool kWs = MODE == kCached || MODE == kCachedTileFj || MODE == kDerive;
       int ch = wave;
       PairPos next = ch < nch ? load_pair_pos(A, S, ch) : PairPos{0.0, 0.0, 0.0};
       while (ch < nch) {
@@ -1362,7 +1407,7 @@ __global__ __launch_bounds__(64 * NW, 1) void k_fused(FusedArgs A) {
     }  // MODE != kRegress
 
     // ---- C: descriptor, head, W ------------------------------------------
-    if constexpr (MODE == kCached || MODE == kRecompute) {
+    if constexpr (MODE == kCached || MODE == kCachedTileFj || MODE == kRecompute) {
       head_stage<K, TM, R, NW, DR, NM, false>(A, S);
     } else if constexpr (MODE == kRegress) {
       head_stage<K, TM, R, NW, DR, NM, true>(A, S);
@@ -1381,7 +1426,16 @@ __global__ __launch_bounds__(64 * NW, 1) void k_fused(FusedArgs A) {
     }
 
     // ---- D: pass 2 ---------------------------------------------------------
-    if constexpr (MODE == kCached || MODE == kDerive) {
+    if constexpr (MODE == kCached || MODE == kCachedTileFj || MODE == kDerive) {
+      constexpr bool kTileFj = MODE == kCachedTileFj;
+      if constexpr (kTileFj) {
+        // the head is done with the union: an empty table for this tile
+        for (int u = tid; u < kFjSlots; u += 64 * NW) {
+          S.u.fj.key[u] = -1;
+          S.u.fj.val[u][0] = S.u.fj.val[u][1] = S.u.fj.val[u][2] = 0.0;
+        }
+        __syncthreads();
+      }
       // inputs of the next chunk are loaded while this one is processed
       int ch = wave;
       Pass2In<K, R> next;
@@ -1390,8 +1444,20 @@ __global__ __launch_bounds__(64 * NW, 1) void k_fused(FusedArgs A) {
         const Pass2In<K, R> cur = next;
         const int ch2 = grab_chunk(&S.next_chunk[1]);
         if (ch2 < nch) pass2_load(A, S, ch2, ws_slot + ch2 * chunk_elems, next);
-        pass2_chunk<K, TM, R, NW, DR, NM>(A, S, ch, cur);
+        pass2_chunk<K, TM, R, NW, DR, NM, kTileFj>(A, S, ch, cur);
         ch = ch2;
+      }
+      if constexpr (kTileFj) {
+        // one atomic per distinct neighbour of the tile instead of one per pair
+        __syncthreads();
+        for (int u = tid; u < kFjSlots; u += 64 * NW) {
+          const int j = S.u.fj.key[u];
+          if (j >= 0) {
+            atomicAdd(&A.forces[3 * (long long)j], S.u.fj.val[u][0]);
+            atomicAdd(&A.forces[3 * (long long)j + 1], S.u.fj.val[u][1]);
+            atomicAdd(&A.forces[3 * (long long)j + 2], S.u.fj.val[u][2]);
+          }
+        }
       }
     } else if constexpr (MODE == kRecompute) {
       // the head's activations overwrote the first-layer weights in LDS
@@ -1412,8 +1478,8 @@ __global__ __launch_bounds__(64 * NW, 1) void k_fused(FusedArgs A) {
     __syncthreads();
 
     // ---- E: outputs --------------------------------------------------------
-    constexpr bool kEnergy = MODE == kCached || MODE == kRecompute || MODE == kRegress;
-    constexpr bool kForces = MODE == kCached || MODE == kRecompute || MODE == kDerive;
+    constexpr bool kEnergy = MODE == kCached || MODE == kCachedTileFj || MODE == kRecompute || MODE == kRegress;
+    constexpr bool kForces = MODE == kCached || MODE == kCachedTileFj || MODE == kRecompute || MODE == kDerive;
     if (tid < na) {
       const long long o = S.orig[tid];
       if (kEnergy && A.energy) A.energy[o] = S.Ei[tid];
@@ -1474,6 +1540,7 @@ hipError_t launch_mode(int mode, const FusedArgs& a, int n_blocks, hipStream_t s
     case kRegress: return launch_k<K, TM, R, NW, DR, NM, kRegress>(a, n_blocks, s);
     case kDerive: return launch_k<K, TM, R, NW, DR, NM, kDerive>(a, n_blocks, s);
     case kRadial: return launch_k<K, TM, R, NW, DR, NM, kRadial>(a, n_blocks, s);
+    case kCachedTileFj: return launch_k<K, TM, R, NW, DR, NM, kCachedTileFj>(a, n_blocks, s);
     default: return hipErrorInvalidValue;
   }
 }

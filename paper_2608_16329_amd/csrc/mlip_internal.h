@@ -183,6 +183,7 @@ struct mlip_ctx {
   int64_t n_tiles = 0;
   int n_blocks = 0;
   int fusion = 0;                   // mlip_fusion
+  int scatter = 0;                  // mlip_scatter
   int acfg = 0;                     // angular configuration of the kernel
   int lrow[8] = {0};                // first angular row of each order
   unsigned char* d_gbuf = nullptr;  // G / dE/dG per atom (three-kernel configuration), cap_gbuf bytes
@@ -233,6 +234,10 @@ hipError_t launch_fused(int k, int precision, int acfg, int mode, const FusedArg
 // Modes of launch_fused used by the unfused configuration.
 constexpr int kModeRegress = 3;   // Eq. 6: G -> E_i, dE/dG
 constexpr int kModeRadial = 5;    // Eq. 2: distances -> g_rad, dg_rad/dr per entry
+// The cached single kernel with the tile-reduced F_j scatter (k = 32,
+// acfg 0): F_j contributions summed per distinct neighbour of a tile in
+// LDS, then one global atomic per neighbour.
+constexpr int kModeCachedTileFj = 6;
 
 // unfused.hip: the other eight kernels of the unfused configuration, in
 // order; k = 32, irreducible basis with l_max <= 3.

@@ -70,8 +70,9 @@ def _unfused_bytes(n_atoms, n_listed, k, lmax, eb):
 
 def test_configurations_agree_and_hold_their_intermediates():
     """The four configurations on one input agree to rounding; the
-    three-kernel one holds (l_max + 1) k values per atom more, the unfused one
-    every intermediate of Eqs. 1-10."""
+    recompute one holds no workspace, the three-kernel one (l_max + 1) k
+    values per atom more than the cached one, the unfused one every
+    intermediate of Eqs. 1-10 and no workspace."""
     w = synth.make_workload("fcc-hea6-128", seed=3, n=6)
     out = {}
     for fusion in (0, 1, 2, 3):
@@ -81,10 +82,13 @@ def test_configurations_agree_and_hold_their_intermediates():
             d = max_abs(out[fusion][key], out[0][key])
             log(f"[fusion] {fusion} vs cached {key}: {d:.2e}")
             assert d <= TOL64
+    st = out[0]["stats"]
+    ws = out[0]["pot"].memory_bytes() - out[1]["pot"].memory_bytes()
+    assert ws > 0 and ws % (8 * st["n_blocks"]) == 0     # one slot per work-group, held by cached only
     extra = out[2]["pot"].memory_bytes() - out[0]["pot"].memory_bytes()
     assert extra == len(w.pos) * (w.hp.lmax + 1) * w.hp.k * 8
     n_listed = out[3]["stats"]["n_listed_pairs"]
-    extra = out[3]["pot"].memory_bytes() - out[0]["pot"].memory_bytes()
+    extra = out[3]["pot"].memory_bytes() - out[1]["pot"].memory_bytes()
     assert extra == _unfused_bytes(len(w.pos), n_listed, w.hp.k, w.hp.lmax, 8)
     for g in out.values():
         g["pot"].close()
@@ -162,3 +166,73 @@ def test_configurations_agree_at_scale(precision):
         assert out[f]["stats"]["n_active_pairs"] == out[0]["stats"]["n_active_pairs"]
     for g in out.values():
         g["pot"].close()
+
+
+def _eval_scatter(hp, weights, pos, types, box, scatter):
+    import torch
+    from paper_2608_16329_amd import Potential
+    pot = Potential(hp, weights)
+    pot.set_scatter(scatter)
+    p = torch.from_numpy(np.ascontiguousarray(pos)).to("cuda:0")
+    t = torch.from_numpy(np.ascontiguousarray(types, dtype=np.int32)).to("cuda:0")
+    pot.build_neighbors(p, t, box)
+    n = len(pos)
+    F = torch.empty((n, 3), dtype=torch.float64, device="cuda:0")
+    E = torch.empty(n, dtype=torch.float64, device="cuda:0")
+    V = torch.empty((n, 9), dtype=torch.float64, device="cuda:0")
+    tot = pot.compute(p, F, E, V, totals=True)
+    torch.cuda.synchronize()
+    out = {"F": F.cpu().numpy(), "E_i": E.cpu().numpy(), "virial": V.cpu().numpy(), "totals": tot,
+           "stats": pot.stats()}
+    pot.close()
+    return out
+
+
+@pytest.mark.parametrize("precision", [64, 32])
+@pytest.mark.parametrize("name,n", [("fcc-binary-4", None), ("fcc-hea6-128", 5), ("bcc-hea6-sweep", 12)])
+def test_tile_reduced_scatter_matches_oracle(precision, name, n):
+    """The F_j scatter summed per distinct neighbour of a tile in LDS (one
+    atomic per neighbour) against the oracle."""
+    w = synth.make_workload(name, seed=19, n=n, hp_overrides={"precision": precision})
+    label = f"{name}/tile scatter/fp{precision}"
+    log(f"[scatter] {label}: N={len(w.pos)}")
+    g = _eval_scatter(w.hp, w.weights, w.pos, w.types, w.box, 1)
+    ref = evaluate(Model(w.hp, w.weights), w.pos, w.types, w.box)
+    if precision == 64:
+        e = [max_abs(g[k], ref[k]) for k in ("E_i", "F", "virial")]
+        log(f"[scatter] {label}: max|dE|={e[0]:.2e} max|dF|={e[1]:.2e} max|dW|={e[2]:.2e}")
+        assert max(e) <= TOL64
+    else:
+        e = [_rel(g[k], ref[k]) for k in ("E_i", "F", "virial")]
+        log(f"[scatter] {label}: rel dE={e[0]:.2e} dF={e[1]:.2e} dW={e[2]:.2e}")
+        assert max(e) <= REL32
+
+
+def test_tile_reduced_scatter_long_rows():
+    """A 12 A cutoff (about 700 neighbours, 2-atom tiles): the tile's table
+    of 1024 slots runs nearly full, and contributions whose probes find no
+    slot take the direct atomic."""
+    rng = np.random.default_rng(31)
+    hp = synth.HParams(n_species=3, cutoff=12.0, skin=0.5)
+    pos, box = synth.lattice("fcc", 7, 3.6)
+    pos = pos + rng.normal(0.0, 0.1, pos.shape)
+    types = rng.integers(0, 3, len(pos)).astype(np.int32)
+    wts = synth.random_weights(hp, 4, 0.3)
+    g = _eval_scatter(hp, wts, pos, types, box, 1)
+    ref = evaluate(Model(hp, wts), pos, types, box)
+    e = [max_abs(g[k], ref[k]) for k in ("E_i", "F", "virial")]
+    log(f"[scatter] long rows: tile {g['stats']['tile_atoms']}, max|dE|={e[0]:.2e} max|dF|={e[1]:.2e} "
+        f"max|dW|={e[2]:.2e}")
+    assert max(e) <= TOL64
+
+
+def test_scatter_argument_checks():
+    from paper_2608_16329_amd import Potential, MlipError
+    hp = synth.HParams(n_species=2, k=16)
+    pot = Potential(hp, synth.random_weights(hp, 0))
+    with pytest.raises(MlipError, match="ARG"):
+        pot.set_scatter(1)
+    with pytest.raises(MlipError, match="ARG"):
+        pot.set_scatter(5)
+    pot.set_scatter(0)
+    pot.close()
