@@ -145,6 +145,10 @@ def summarize_traffic(fetch_dir: str, write_dir: str, bench_log: str, copy_bytes
         else:
             f.write("This configuration keeps no workspace: the traffic is neighbour positions, neighbour-list "
                     "entries, encoder weights missing L2, and the outputs. ")
+        atomics = 3.0 * b["config"]["active_pairs_per_atom"] * b["config"]["n_atoms"]
+        f.write(f"WRITE_SIZE counts each float64 atomic add of the force scatter (F_j -= f_ij, three per active "
+                f"pair, {atomics:.3g} per launch) as a 32-byte write, {32 * atomics / 1e9:.1f} GB of the written "
+                f"figure, although each carries 8 bytes. ")
         f.write("The counters see L2-to-fabric requests, which include Infinity Cache hits: no counter of this "
                 "part separates Infinity Cache hits from HBM accesses.\n\n")
         f.write("traffic_json: " + json.dumps(t) + "\n")
