@@ -96,6 +96,7 @@ typedef struct {
   int32_t n_cells;          /* cells of the neighbour grid                       */
   int64_t n_builds;         /* neighbour builds so far                           */
   size_t  device_bytes;     /* device memory held by the context                 */
+  int32_t list_entry_bytes; /* bytes per neighbour-list entry: 2 (coded), 4      */
 } mlip_stats;
 
 /*
@@ -137,6 +138,11 @@ mlip_status mlip_create(const mlip_hparams* hp, const double* weights_host, size
  * vector dx = w_j - w_i folded once by -L if dx > L/2 or +L if dx < -L/2;
  * d2 = (dx*dx + dy*dy) + dz*dz without fused multiply-add; j != i is listed
  * iff d2 < (cutoff + skin)^2.  Rows are grouped by neighbour species.
+ * Entries take 2 bytes each (the neighbour's place among the cells scanned
+ * around the centre's cell, its species and its place in that cell's
+ * species bucket) when every (species, cell) bucket of the cell grid holds at
+ * most 2^(11 - ceil(log2 C)) atoms, 4 bytes (its index) otherwise or when
+ * mlip_set_list_format asks for indices; mlip_get_stats reports which.
  *   n_atoms   number of atoms (>= 0, < 2^31).  0 records an empty system
  *             (the pointers may then be NULL): later calls succeed and
  *             produce nothing, totals and kinetic energy 0
@@ -278,6 +284,15 @@ mlip_status mlip_set_fusion(mlip_ctx* ctx, int32_t fusion);
  */
 typedef enum { MLIP_SCATTER_ATOMIC = 0, MLIP_SCATTER_TILE = 1 } mlip_scatter;
 mlip_status mlip_set_scatter(mlip_ctx* ctx, int32_t scatter);
+
+/*
+ * Encoding of the neighbour list's entries from the next mlip_build_neighbors
+ * on: MLIP_LIST_AUTO (default) codes entries in 2 bytes whenever the cell
+ * grid's buckets allow it, MLIP_LIST_INDEX always stores 4-byte indices.
+ * Both give the same neighbour sets and results.  Errors: MLIP_E_ARG.
+ */
+typedef enum { MLIP_LIST_AUTO = 0, MLIP_LIST_INDEX = 1 } mlip_list_format;
+mlip_status mlip_set_list_format(mlip_ctx* ctx, int32_t format);
 
 /* Device memory held by the context, in bytes. */
 mlip_status mlip_memory_bytes(const mlip_ctx* ctx, size_t* bytes);

@@ -71,6 +71,11 @@ class Potential:
         """binding.MLIP_SCATTER_ATOMIC (default) or MLIP_SCATTER_TILE."""
         binding.mlip_set_scatter(self.ctx, scatter)
 
+    def set_list_format(self, fmt: int) -> None:
+        """binding.MLIP_LIST_AUTO (2-byte coded entries where possible, default)
+        or MLIP_LIST_INDEX (4-byte indices); applies from the next build."""
+        binding.mlip_set_list_format(self.ctx, fmt)
+
     def neighbors(self):
         return binding.mlip_get_neighbors(self.ctx)
 

@@ -25,12 +25,13 @@ STATUS = {0: "MLIP_OK", -1: "MLIP_E_ARG", -2: "MLIP_E_OOM", -3: "MLIP_E_HIP", -4
 EXPORTED = ["mlip_weight_count", "mlip_create", "mlip_build_neighbors", "mlip_compute", "mlip_get_neighbors",
             "mlip_memory_bytes", "mlip_get_stats", "mlip_last_error", "mlip_destroy", "mlip_md_set_masses",
             "mlip_md_first_half", "mlip_md_second_half", "mlip_md_kinetic", "mlip_set_fusion",
-            "mlip_get_neighbor_rows", "mlip_compute_noalloc", "mlip_set_scatter"]
+            "mlip_get_neighbor_rows", "mlip_compute_noalloc", "mlip_set_scatter", "mlip_set_list_format"]
 
 MLIP_STATIC_SCRATCH_BYTES = 256 * 1024 * 1024
 
 MLIP_FUSION_CACHED, MLIP_FUSION_RECOMPUTE, MLIP_FUSION_PARTIAL, MLIP_FUSION_UNFUSED = 0, 1, 2, 3
 MLIP_SCATTER_ATOMIC, MLIP_SCATTER_TILE = 0, 1
+MLIP_LIST_AUTO, MLIP_LIST_INDEX = 0, 1
 
 
 class mlip_hparams(ctypes.Structure):
@@ -45,7 +46,8 @@ class mlip_stats(ctypes.Structure):
     _fields_ = [("n_atoms", ctypes.c_int64), ("n_listed_pairs", ctypes.c_int64),
                 ("n_active_pairs", ctypes.c_int64), ("max_row", ctypes.c_int32), ("tile_atoms", ctypes.c_int32),
                 ("n_tiles", ctypes.c_int64), ("n_blocks", ctypes.c_int32), ("n_cells", ctypes.c_int32),
-                ("n_builds", ctypes.c_int64), ("device_bytes", ctypes.c_size_t)]
+                ("n_builds", ctypes.c_int64), ("device_bytes", ctypes.c_size_t),
+                ("list_entry_bytes", ctypes.c_int32)]
 
     def as_dict(self):
         return {name: getattr(self, name) for name, _ in self._fields_}
@@ -83,6 +85,7 @@ def _load() -> ctypes.CDLL:
         "mlip_md_kinetic": (st, [vp, vp, dp]),
         "mlip_set_fusion": (st, [vp, ctypes.c_int32]),
         "mlip_set_scatter": (st, [vp, ctypes.c_int32]),
+        "mlip_set_list_format": (st, [vp, ctypes.c_int32]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -179,6 +182,10 @@ def mlip_set_fusion(ctx: int, fusion: int) -> None:
 
 def mlip_set_scatter(ctx: int, scatter: int) -> None:
     _check(ctx, _lib.mlip_set_scatter(ctx, int(scatter)))
+
+
+def mlip_set_list_format(ctx: int, fmt: int) -> None:
+    _check(ctx, _lib.mlip_set_list_format(ctx, int(fmt)))
 
 
 def mlip_memory_bytes(ctx: int) -> int:

@@ -7,6 +7,7 @@
 #include <string>
 #include <vector>
 
+#include "kernel_math.h"
 #include "mlip_internal.h"
 
 using namespace mlip;
@@ -151,6 +152,60 @@ std::vector<double> transpose(const double* M, int rows, int cols) {
   return t;
 }
 
+// The neighbour list as the kernels read it (ListView).
+ListView list_view(const mlip_ctx* ctx) {
+  ListView v{};
+  v.idx32 = ctx->list_compact ? nullptr : reinterpret_cast<const int32_t*>(ctx->d_idx);
+  v.idx16 = ctx->list_compact ? reinterpret_cast<const uint16_t*>(ctx->d_idx) : nullptr;
+  v.start = ctx->d_cell_start;
+  v.perm = ctx->d_perm;
+  v.key = ctx->d_key;
+  for (int d = 0; d < 3; ++d) v.nc[d] = ctx->grid.nc[d];
+  v.ncell = ctx->grid.ncell;
+  v.tbits = ctx->list_tbits;
+  v.sbits = ctx->list_sbits;
+  return v;
+}
+
+// Host copies of what decoding coded entries needs (bucket starts,
+// permutation, keys), and a ListView over them.
+struct HostList {
+  std::vector<int32_t> start, perm, key;
+  ListView view{};
+};
+
+mlip_status host_list(mlip_ctx* ctx, HostList* h) {
+  h->view = list_view(ctx);
+  h->view.idx32 = nullptr;
+  h->view.idx16 = nullptr;
+  if (!ctx->list_compact) return MLIP_OK;
+  const size_t n = size_t(ctx->n), nkeys = size_t(ctx->grid.ncell) * size_t(ctx->hp.n_species) + 1;
+  h->start.resize(nkeys);
+  h->perm.resize(n);
+  h->key.resize(n);
+  MLIP_HIP(ctx, hipMemcpy(h->start.data(), ctx->d_cell_start, nkeys * sizeof(int32_t), hipMemcpyDeviceToHost));
+  MLIP_HIP(ctx, hipMemcpy(h->perm.data(), ctx->d_perm, n * sizeof(int32_t), hipMemcpyDeviceToHost));
+  MLIP_HIP(ctx, hipMemcpy(h->key.data(), ctx->d_key, n * sizeof(int32_t), hipMemcpyDeviceToHost));
+  h->view.start = h->start.data();
+  h->view.perm = h->perm.data();
+  h->view.key = h->key.data();
+  return MLIP_OK;
+}
+
+// Caller indices of entries [beg, beg + len) of the row of caller atom i,
+// from a host copy of those entries (int32 or codes).
+void decode_row(const mlip_ctx* ctx, const HostList& h, int64_t i, const unsigned char* entries, int64_t len,
+                int32_t* out) {
+  if (!ctx->list_compact) {
+    std::memcpy(out, entries, size_t(len) * sizeof(int32_t));
+    return;
+  }
+  int cand[9];
+  centre_cells(h.view, h.key[size_t(i)], cand);
+  const uint16_t* codes = reinterpret_cast<const uint16_t*>(entries);
+  for (int64_t e = 0; e < len; ++e) out[e] = h.view.perm[code_slot(h.view, cand, codes[e])];
+}
+
 // Copy the totals to the host when asked (synchronising the stream).
 mlip_status finish_compute(mlip_ctx* ctx, const double* d_totals, double* totals_host) {
   if (totals_host) {
@@ -205,7 +260,7 @@ mlip_status compute_unfused(mlip_ctx* ctx, FusedArgs& a) {
   u.pos = a.pos;
   u.perm = ctx->d_perm;
   u.offsets = ctx->d_offsets;
-  u.idx = ctx->d_idx;
+  u.list = list_view(ctx);
   u.qc = ctx->d_qc;
   u.geo = reinterpret_cast<double*>(p[0]);
   u.grad = p[1];
@@ -267,7 +322,7 @@ mlip_status run_compute(mlip_ctx* ctx, const double* pos_dev, double* energy_dev
   a.types = ctx->d_types;
   a.perm = ctx->d_perm;
   a.offsets = ctx->d_offsets;
-  a.idx = ctx->d_idx;
+  a.list = list_view(ctx);
   a.enc = ctx->d_enc;
   a.head = ctx->d_head;
   a.qc = ctx->d_qc;
@@ -518,11 +573,11 @@ mlip_status mlip_build_neighbors(mlip_ctx* ctx, int64_t n_atoms, const double* p
   MLIP_HIP(ctx, launch_bin(pos_dev, ctx->d_types, n, g, ctx->d_key, ctx->d_cell_count, ctx->d_flags, s));
   MLIP_HIP(ctx, launch_exclusive_scan_i32_to_i32(ctx->d_cell_count, nkeys, ctx->d_cell_start, ctx->d_scan_tmp, s));
   MLIP_HIP(ctx, launch_fill_i32(ctx->d_cell_count, nkeys + 1, 0, s));
-  MLIP_HIP(ctx, launch_scatter(ctx->d_key, n, ctx->d_cell_start, ctx->d_cell_count, ctx->d_perm, s));
+  MLIP_HIP(ctx, launch_scatter(ctx->d_key, n, ctx->d_cell_start, ctx->d_cell_count, ctx->d_perm, ctx->d_flags, s));
   MLIP_HIP(ctx, launch_sort_segments(ctx->d_cell_start, nkeys, ctx->d_perm, s));
   MLIP_HIP(ctx, launch_gather_sorted(pos_dev, ctx->d_perm, n, g, ctx->d_spos, s));
   MLIP_HIP(ctx, launch_rows(ctx->d_spos, ctx->d_perm, n, g, ctx->d_cell_start, ctx->d_rowcnt, nullptr, nullptr,
-                            ctx->d_flags, false, s));
+                            ctx->d_flags, false, 0, 0, s));
   MLIP_HIP(ctx, launch_exclusive_scan_i32_to_i64(ctx->d_rowcnt, n, ctx->d_offsets, ctx->d_scan_tmp, s));
 
   int64_t total = 0;
@@ -537,7 +592,16 @@ mlip_status mlip_build_neighbors(mlip_ctx* ctx, int64_t n_atoms, const double* p
   if (flags[0]) return fail(ctx, MLIP_E_TYPE, "species outside [0, n_species) or non-finite position");
   if (flags[1] > kEntCap) return fail(ctx, MLIP_E_NBR_CAP, "a neighbour row is longer than 2048 entries");
 
-  size_t need = size_t(std::max<int64_t>(total, 1));
+  // entries as 16-bit codes (cell choice, species, place in the bucket) when
+  // every (species, cell) bucket fits the place field, else int32 indices
+  int sbits = 0;
+  while ((1 << sbits) < C) ++sbits;
+  const int tbits = 11 - sbits;
+  ctx->list_compact = !ctx->force_wide_list && flags[2] <= (1 << tbits);
+  ctx->list_tbits = ctx->list_compact ? tbits : 0;
+  ctx->list_sbits = ctx->list_compact ? sbits : 0;
+  const size_t entry_bytes = ctx->list_compact ? sizeof(uint16_t) : sizeof(int32_t);
+  size_t need = size_t(std::max<int64_t>(total, 1)) * entry_bytes;
   // 1/32 headroom for later builds: in MD the list length drifts by well under
   // that between rebuilds, and every byte of slack is a byte per entry that
   // the largest system cannot use (the old buffer is freed before the new one
@@ -545,7 +609,7 @@ mlip_status mlip_build_neighbors(mlip_ctx* ctx, int64_t n_atoms, const double* p
   if (need > ctx->cap_idx) need = need + need / 32;
   MLIP_TRY(ensure(ctx, &ctx->d_idx, &ctx->cap_idx, need, "neighbour list"));
   MLIP_HIP(ctx, launch_rows(ctx->d_spos, ctx->d_perm, n, g, ctx->d_cell_start, ctx->d_rowcnt, ctx->d_offsets,
-                            ctx->d_idx, ctx->d_flags, true, s));
+                            ctx->d_idx, ctx->d_flags, true, ctx->list_tbits, ctx->list_sbits, s));
 
   ctx->grid = g;
   ctx->n = n;
@@ -622,21 +686,24 @@ mlip_status mlip_get_neighbors(mlip_ctx* ctx, int64_t* offsets_host, int32_t* id
     offsets_host[0] = 0;
     return MLIP_OK;
   }
+  const size_t eb = ctx->list_compact ? sizeof(uint16_t) : sizeof(int32_t);
   std::vector<int64_t> off(size_t(n + 1));
   std::vector<int32_t> perm(static_cast<size_t>(n));
-  std::vector<int32_t> idx(static_cast<size_t>(std::max<int64_t>(ctx->n_listed, 1)));
+  std::vector<unsigned char> ent(size_t(std::max<int64_t>(ctx->n_listed, 1)) * eb);
   MLIP_HIP(ctx, hipStreamSynchronize(ctx->stream));
   MLIP_HIP(ctx, hipMemcpy(off.data(), ctx->d_offsets, off.size() * sizeof(int64_t), hipMemcpyDeviceToHost));
   MLIP_HIP(ctx, hipMemcpy(perm.data(), ctx->d_perm, perm.size() * sizeof(int32_t), hipMemcpyDeviceToHost));
   if (ctx->n_listed > 0)
-    MLIP_HIP(ctx, hipMemcpy(idx.data(), ctx->d_idx, size_t(ctx->n_listed) * sizeof(int32_t), hipMemcpyDeviceToHost));
+    MLIP_HIP(ctx, hipMemcpy(ent.data(), ctx->d_idx, size_t(ctx->n_listed) * eb, hipMemcpyDeviceToHost));
+  HostList h;
+  MLIP_TRY(host_list(ctx, &h));
   std::vector<int64_t> len(size_t(n), 0);
   for (int64_t a = 0; a < n; ++a) len[size_t(perm[size_t(a)])] = off[size_t(a + 1)] - off[size_t(a)];
   offsets_host[0] = 0;
   for (int64_t i = 0; i < n; ++i) offsets_host[i + 1] = offsets_host[i] + len[size_t(i)];
   for (int64_t a = 0; a < n; ++a) {
     const int64_t i = perm[size_t(a)];
-    std::memcpy(idx_host + offsets_host[i], idx.data() + off[size_t(a)], size_t(len[size_t(i)]) * sizeof(int32_t));
+    decode_row(ctx, h, i, ent.data() + size_t(off[size_t(a)]) * eb, len[size_t(i)], idx_host + offsets_host[i]);
   }
   return MLIP_OK;
 }
@@ -673,12 +740,32 @@ mlip_status mlip_get_neighbor_rows(mlip_ctx* ctx, const int64_t* atoms_host, int
     total += counts_host[r];
   }
   if (total > cap) return fail(ctx, MLIP_E_ARG, "the rows do not fit in cap entries");
+  // bucket starts for decoding, and each requested atom's key
+  HostList h;
+  h.view = list_view(ctx);
+  if (ctx->list_compact) {
+    const size_t nkeys = size_t(ctx->grid.ncell) * size_t(ctx->hp.n_species) + 1;
+    h.start.resize(nkeys);
+    MLIP_HIP(ctx, hipMemcpy(h.start.data(), ctx->d_cell_start, nkeys * sizeof(int32_t), hipMemcpyDeviceToHost));
+    h.view.start = h.start.data();
+    h.view.perm = perm.data();
+    h.key.assign(size_t(n), 0);
+    for (int64_t r = 0; r < n_rows; ++r)
+      MLIP_HIP(ctx, hipMemcpy(&h.key[size_t(atoms_host[r])], ctx->d_key + atoms_host[r], sizeof(int32_t),
+                              hipMemcpyDeviceToHost));
+  }
+  const size_t eb = ctx->list_compact ? sizeof(uint16_t) : sizeof(int32_t);
+  std::vector<unsigned char> ent;
   int64_t at = 0;
   for (int64_t r = 0; r < n_rows; ++r) {
-    if (counts_host[r] > 0)
-      MLIP_HIP(ctx, hipMemcpy(idx_host + at, ctx->d_idx + beg[size_t(r)], size_t(counts_host[r]) * sizeof(int32_t),
+    const int64_t len = counts_host[r];
+    if (len > 0) {
+      ent.resize(size_t(len) * eb);
+      MLIP_HIP(ctx, hipMemcpy(ent.data(), ctx->d_idx + size_t(beg[size_t(r)]) * eb, size_t(len) * eb,
                               hipMemcpyDeviceToHost));
-    at += counts_host[r];
+      decode_row(ctx, h, atoms_host[r], ent.data(), len, idx_host + at);
+    }
+    at += len;
   }
   return MLIP_OK;
 }
@@ -722,6 +809,14 @@ mlip_status mlip_set_scatter(mlip_ctx* ctx, int32_t scatter) {
   return MLIP_OK;
 }
 
+mlip_status mlip_set_list_format(mlip_ctx* ctx, int32_t format) {
+  if (!ctx) return MLIP_E_ARG;
+  ctx->err.clear();
+  if (format != MLIP_LIST_AUTO && format != MLIP_LIST_INDEX) return fail(ctx, MLIP_E_ARG, "unknown list format");
+  ctx->force_wide_list = format == MLIP_LIST_INDEX;
+  return MLIP_OK;
+}
+
 mlip_status mlip_memory_bytes(const mlip_ctx* ctx, size_t* bytes) {
   if (!ctx || !bytes) return MLIP_E_ARG;
   *bytes = ctx->bytes;
@@ -746,6 +841,7 @@ mlip_status mlip_get_stats(mlip_ctx* ctx, mlip_stats* st) {
   st->n_cells = ctx->grid.ncell;
   st->n_builds = ctx->n_builds;
   st->device_bytes = ctx->bytes;
+  st->list_entry_bytes = ctx->n > 0 ? (ctx->list_compact ? 2 : 4) : 0;
   return MLIP_OK;
 }
 

@@ -274,6 +274,7 @@ struct Smem {
   long long row_beg[TM];
   int ent_base[TM + 1];
   int orig[TM];
+  int cand[TM][9];     // cells scanned around each atom's cell (decoding coded list entries)
   int cnt[kMaxSpecies][TM];
   int base[kMaxSpecies][TM];
   int pair_j[tile_entry_cap(TM)];
@@ -1243,6 +1244,7 @@ __global__ __launch_bounds__(64 * NW, 1) void k_fused(FusedArgs A) {
       if (tid < na) {
         const int o = A.perm[a0 + tid];
         S.orig[tid] = o;
+        if (A.list.idx16) centre_cells(A.list, A.list.key[o], S.cand[tid]);
         S.tpos[tid][0] = A.pos[3 * (long long)o];
         S.tpos[tid][1] = A.pos[3 * (long long)o + 1];
         S.tpos[tid][2] = A.pos[3 * (long long)o + 2];
@@ -1275,12 +1277,29 @@ __global__ __launch_bounds__(64 * NW, 1) void k_fused(FusedArgs A) {
       int a = 0;
       while (a + 1 < na && e0 >= S.ent_base[a + 1]) ++a;
 #pragma unroll
-      for (int k = 0; k < kPer; ++k) ej[k] = e0 + k < nent ? A.idx[ebase + e0 + k] : -1;
+      for (int k = 0; k < kPer; ++k) {
+        while (a + 1 < na && e0 + k >= S.ent_base[a + 1]) ++a;
+        ea[k] = a;
+      }
+      if (A.list.idx32) {
+#pragma unroll
+        for (int k = 0; k < kPer; ++k) ej[k] = e0 + k < nent ? A.list.idx32[ebase + e0 + k] : -1;
+      } else {
+        // coded entries: bucket start through the centre's candidate cells,
+        // then the permutation (each level's loads issued together)
+        unsigned code[kPer];
+        int slot[kPer];
+#pragma unroll
+        for (int k = 0; k < kPer; ++k) code[k] = e0 + k < nent ? A.list.idx16[ebase + e0 + k] : 0u;
+#pragma unroll
+        for (int k = 0; k < kPer; ++k) slot[k] = e0 + k < nent ? code_slot(A.list, S.cand[ea[k]], code[k]) : -1;
+#pragma unroll
+        for (int k = 0; k < kPer; ++k) ej[k] = slot[k] >= 0 ? A.list.perm[slot[k]] : -1;
+      }
 #pragma unroll
       for (int k = 0; k < kPer; ++k) {
         const int e = e0 + k;
-        while (a + 1 < na && e >= S.ent_base[a + 1]) ++a;
-        ea[k] = a;
+        a = ea[k];
         es[k] = -1;
         const int j = ej[k];
         if (j >= 0) {

@@ -12,6 +12,48 @@ namespace mlip {
 // Minimum-image fold of one coordinate difference (Eq. 1 in a periodic box).
 __device__ __forceinline__ double fold(double d, double L, double invL) { return d - L * rint(d * invL); }
 
+// The cells scanned around cell c in a dimension of nc cells, in scan order:
+// c-1, c, c+1 (periodic) when nc >= 3, all cells otherwise.  Shared by the
+// list builder and every reader of coded entries.
+__host__ __device__ __forceinline__ void nbr_cells(int c, int nc, int out[3]) {
+  if (nc >= 3) {
+    out[0] = c == 0 ? nc - 1 : c - 1;
+    out[1] = c;
+    out[2] = c == nc - 1 ? 0 : c + 1;
+  } else {
+    out[0] = 0;
+    out[1] = nc == 2 ? 1 : 0;
+    out[2] = out[1];
+  }
+}
+
+// The 3 x 3 candidate cells of a centre atom from its bucket key:
+// cand[0..2] along x, [3..5] along y, [6..8] along z.
+__host__ __device__ __forceinline__ void centre_cells(const ListView& L, int key, int cand[9]) {
+  const int cell = key % L.ncell;
+  const int cx = cell % L.nc[0], cy = (cell / L.nc[0]) % L.nc[1], cz = cell / (L.nc[0] * L.nc[1]);
+  nbr_cells(cx, L.nc[0], cand);
+  nbr_cells(cy, L.nc[1], cand + 3);
+  nbr_cells(cz, L.nc[2], cand + 6);
+}
+
+// Sorted slot of a coded entry of a centre with candidate cells cand.
+__host__ __device__ __forceinline__ int code_slot(const ListView& L, const int cand[9], unsigned code) {
+  const int t = int(code & ((1u << L.tbits) - 1u));
+  const int sp = int((code >> L.tbits) & ((1u << L.sbits) - 1u));
+  const int o = int(code >> (L.tbits + L.sbits));
+  const int ix = o % 3, iy = (o / 3) % 3, iz = o / 9;
+  const int key = sp * L.ncell + (cand[6 + iz] * L.nc[1] + cand[3 + iy]) * L.nc[0] + cand[ix];
+  return L.start[key] + t;
+}
+
+// Caller index of neighbour-list entry e of a centre (cand from centre_cells);
+// the host readers of the list use it on host copies of the arrays.
+__host__ __device__ __forceinline__ int list_entry(const ListView& L, const int cand[9], long long e) {
+  if (L.idx32) return L.idx32[e];
+  return L.perm[code_slot(L, cand, L.idx16[e])];
+}
+
 // Cartesian monomials of degree <= 3 in the order of the angular table
 // (degree by degree, lexicographic with x first).
 template <typename R>

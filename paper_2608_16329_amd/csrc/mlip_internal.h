@@ -43,13 +43,33 @@ inline size_t head_table_elems(int nin, int reg_hidden) {
          size_t(reg_hidden - 1) * (2 * kHeadWidth * kHeadWidth + kHeadWidth) + kHeadWidth + 1;
 }
 
+// The neighbour list's entries: caller indices (int32), or 16-bit codes.  A
+// code names the neighbour by where the builder found it: which of the up to
+// 27 cells scanned around the centre's cell (the index ix + 3 iy + 9 iz into
+// the per-dimension candidate lists of `nbr_cells`), the neighbour's species
+// s, and its place t in the (s, cell) bucket of the sorted order:
+//   code = ((9 iz + 3 iy + ix) << (sbits + tbits)) | (s << tbits) | t,
+// sbits = bits of C - 1, tbits = 11 - sbits (27 < 2^5).  The caller index is
+// perm[start[s ncell + cell] + t].  The builder writes codes when every
+// bucket holds at most 2^tbits atoms, int32 indices otherwise.
+struct ListView {
+  const int32_t* idx32;       // caller indices (null when the list is coded)
+  const uint16_t* idx16;      // codes (null when the list holds indices)
+  const int32_t* start;       // [C ncell + 1] first sorted slot of each (species, cell) bucket
+  const int32_t* perm;        // sorted slot -> caller index
+  const int32_t* key;         // caller index -> bucket key s ncell + cell at the last build
+  int nc[3];                  // cells per dimension
+  int ncell;
+  int tbits, sbits;
+};
+
 // Arguments of the fused energy/force/virial kernel.
 struct FusedArgs {
   const double* pos;          // caller order [n][3]
   const int32_t* types;       // caller order [n] (library copy)
   const int32_t* perm;        // sorted slot -> caller index
   const int64_t* offsets;     // [n+1], rows in sorted order
-  const int32_t* idx;         // neighbour entries, caller indices
+  ListView list;              // neighbour entries
   // network tables and workspace hold the kernel's arithmetic type
   // (float64 or float32, mlip_hparams.precision)
   const void* enc;            // packed encoder tables
@@ -90,7 +110,7 @@ struct UnfusedArgs {
   const double* pos;          // caller order [n][3]
   const int32_t* perm;        // sorted slot -> caller index
   const int64_t* offsets;     // [n+1]
-  const int32_t* idx;         // neighbour entries, caller indices
+  ListView list;              // neighbour entries
   const void* qc;             // angular table [16][20], then the row metric [16]
   double* geo;                // [entries][4]: dx, dy, dz, r (r = -1 beyond the cutoff)
   const void* grad;           // [entries][k]  g_rad (written by the radial kernel)
@@ -158,8 +178,11 @@ struct mlip_ctx {
   double* d_spos = nullptr;
   int32_t* d_rowcnt = nullptr;
   int64_t* d_offsets = nullptr;
-  int32_t* d_idx = nullptr;
-  size_t cap_idx = 0;
+  unsigned char* d_idx = nullptr;   // entries: uint16 codes or int32 indices (list_compact)
+  size_t cap_idx = 0;               // bytes
+  bool list_compact = false;
+  bool force_wide_list = false;     // mlip_set_list_format(MLIP_LIST_INDEX)
+  int list_tbits = 0, list_sbits = 0;
   int32_t* d_cell_count = nullptr;
   int32_t* d_cell_start = nullptr;
   size_t cap_keys = 0;
@@ -205,13 +228,15 @@ bool build_angular_table(int lmax, int angular, int rows, int cols, std::vector<
 hipError_t launch_bin(const double* pos, const int32_t* types, int64_t n, const NbrGrid& g,
                       int32_t* key, int32_t* cell_count, int32_t* flags, hipStream_t s);
 hipError_t launch_scatter(const int32_t* key, int64_t n, const int32_t* cell_start, int32_t* fill,
-                          int32_t* perm, hipStream_t s);
+                          int32_t* perm, int32_t* flags, hipStream_t s);
 hipError_t launch_sort_segments(const int32_t* cell_start, int64_t nkeys, int32_t* perm, hipStream_t s);
 hipError_t launch_gather_sorted(const double* pos, const int32_t* perm, int64_t n, const NbrGrid& g,
                                 double* spos, hipStream_t s);
+// rows: count pass (fill false) or fill pass writing int32 indices or, with
+// tbits > 0, 16-bit codes (ListView) into idx
 hipError_t launch_rows(const double* spos, const int32_t* perm, int64_t n, const NbrGrid& g,
-                       const int32_t* cell_start, int32_t* rowcnt, const int64_t* offsets, int32_t* idx,
-                       int32_t* flags, bool fill, hipStream_t s);
+                       const int32_t* cell_start, int32_t* rowcnt, const int64_t* offsets, void* idx,
+                       int32_t* flags, bool fill, int tbits, int sbits, hipStream_t s);
 hipError_t launch_exclusive_scan_i32_to_i32(const int32_t* in, int64_t n, int32_t* out, int64_t* tmp,
                                             hipStream_t s);
 hipError_t launch_exclusive_scan_i32_to_i64(const int32_t* in, int64_t n, int64_t* out, int64_t* tmp,

@@ -9,6 +9,7 @@
 // species.  The distance test is the exact one of the library's contract:
 // wrapped coordinates, one minimum-image fold, (dx*dx + dy*dy) + dz*dz with
 // round-to-nearest products and sums (no contraction), strict comparison.
+#include "kernel_math.h"
 #include "mlip_internal.h"
 
 namespace mlip {
@@ -30,24 +31,21 @@ __device__ inline int cell_of(double w, double scale, int nc) {
   return c < nc ? c : nc - 1;
 }
 
-// Distinct periodic neighbours of cell c in a dimension of nc cells.
+// Distinct periodic neighbours of cell c in a dimension of nc cells, in the
+// order the coded entries refer to (nbr_cells); returns how many.
 __device__ inline int adjacent(int c, int nc, int out[3]) {
-  if (nc == 1) {
-    out[0] = 0;
-    return 1;
-  }
-  if (nc == 2) {
-    out[0] = 0;
-    out[1] = 1;
-    return 2;
-  }
-  out[0] = c == 0 ? nc - 1 : c - 1;
-  out[1] = c;
-  out[2] = c == nc - 1 ? 0 : c + 1;
-  return 3;
+  nbr_cells(c, nc, out);
+  return nc >= 3 ? 3 : nc;
 }
 
-__device__ inline double fold(double d, double L, double h) {
+// Largest value over the wavefront (every lane active), applied by its first
+// lane with one atomic.
+__device__ inline void wave_atomic_max(int32_t* dst, int v) {
+  for (int o = 32; o > 0; o >>= 1) v = max(v, __shfl_xor(v, o, 64));
+  if ((threadIdx.x & 63) == 0) atomicMax(dst, v);
+}
+
+__device__ inline double fold_half(double d, double L, double h) {
   if (d > h) return d - L;
   if (d < -h) return d + L;
   return d;
@@ -78,13 +76,19 @@ __global__ void k_bin(const double* __restrict__ pos, const int32_t* __restrict_
   atomicAdd(&cell_count[k], 1);
 }
 
+// Counting-sort scatter; flags[2] receives the largest bucket (which decides
+// whether entries fit the 16-bit code).
 __global__ void k_scatter(const int32_t* __restrict__ key, int64_t n, const int32_t* __restrict__ start,
-                          int32_t* __restrict__ fill, int32_t* __restrict__ perm) {
+                          int32_t* __restrict__ fill, int32_t* __restrict__ perm, int32_t* __restrict__ flags) {
   const int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
-  if (i >= n) return;
-  const int k = key[i];
-  const int slot = start[k] + atomicAdd(&fill[k], 1);
-  perm[slot] = int32_t(i);
+  if ((i & ~int64_t(63)) >= n) return;  // the whole wavefront is past the end
+  int place = 0;
+  if (i < n) {
+    const int k = key[i];
+    place = atomicAdd(&fill[k], 1);
+    perm[start[k] + place] = int32_t(i);
+  }
+  wave_atomic_max(&flags[2], place + 1);
 }
 
 // Make the order inside each (species, cell) bucket deterministic.
@@ -113,13 +117,21 @@ __global__ void k_gather_sorted(const double* __restrict__ pos, const int32_t* _
   spos[3 * a + 2] = wrap1(pos[3 * i + 2], g.box[2]);
 }
 
-template <bool kFill>
+// Rows by a 27-cell scan: the count pass (kFill false) records row lengths,
+// the fill pass writes caller indices or, with kCode, 16-bit codes (ListView):
+// a candidate's code names the scanned cell it sits in (tracked along each
+// run of consecutive cells), its species and its place in that bucket.
+template <bool kFill, bool kCode>
 __global__ void k_rows(const double* __restrict__ spos, const int32_t* __restrict__ perm, int64_t n, NbrGrid g,
                        const int32_t* __restrict__ start, int32_t* __restrict__ rowcnt,
-                       const int64_t* __restrict__ offsets, int32_t* __restrict__ idx,
-                       int32_t* __restrict__ flags) {
-  const int64_t a = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
-  if (a >= n) return;
+                       const int64_t* __restrict__ offsets, void* __restrict__ idx,
+                       int32_t* __restrict__ flags, int tbits, int sbits) {
+  const int64_t a0 = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+  if ((a0 & ~int64_t(63)) >= n) return;  // the whole wavefront is past the end
+  if (kFill && a0 >= n) return;
+  // count pass: lanes past the end repeat the last atom so that every lane
+  // joins the wavefront's maximum
+  const int64_t a = a0 < n ? a0 : n - 1;
   const double wx = spos[3 * a], wy = spos[3 * a + 1], wz = spos[3 * a + 2];
   int xs[3], ys[3], zs[3];
   const int nx = adjacent(cell_of(wx, g.cell_scale[0], g.nc[0]), g.nc[0], xs);
@@ -135,6 +147,7 @@ __global__ void k_rows(const double* __restrict__ spos, const int32_t* __restric
         // (same entries in the same order)
         int ix = 0;
         while (ix < nx) {
+          const int ix0 = ix;
           const int x0 = xs[ix];
           int x1 = x0;
           while (ix + 1 < nx && xs[ix + 1] == x1 + 1) {
@@ -144,13 +157,29 @@ __global__ void k_rows(const double* __restrict__ spos, const int32_t* __restric
           ++ix;
           const int key = s * g.ncell + (zs[iz] * g.nc[1] + ys[iy]) * g.nc[0] + x0;
           const int e = start[key + (x1 - x0) + 1];
+          int cur = 0;                   // cell x0 + cur of the run holds slot b
+          int cell_end = start[key + 1];
           for (int b = start[key]; b < e; ++b) {
+            if (kCode)
+              while (b >= cell_end) {
+                ++cur;
+                cell_end = start[key + cur + 1];
+              }
             if (b == a) continue;
-            const double dx = fold(spos[3 * int64_t(b)] - wx, g.box[0], g.half[0]);
-            const double dy = fold(spos[3 * int64_t(b) + 1] - wy, g.box[1], g.half[1]);
-            const double dz = fold(spos[3 * int64_t(b) + 2] - wz, g.box[2], g.half[2]);
+            const double dx = fold_half(spos[3 * int64_t(b)] - wx, g.box[0], g.half[0]);
+            const double dy = fold_half(spos[3 * int64_t(b) + 1] - wy, g.box[1], g.half[1]);
+            const double dz = fold_half(spos[3 * int64_t(b) + 2] - wz, g.box[2], g.half[2]);
             if (sqdist(dx, dy, dz) < g.rl2) {
-              if (kFill) idx[base + cnt] = perm[b];
+              if (kFill) {
+                if constexpr (kCode) {
+                  const unsigned o = unsigned((iz * 3 + iy) * 3 + ix0 + cur);
+                  const unsigned t = unsigned(b - start[key + cur]);
+                  static_cast<uint16_t*>(idx)[base + cnt] =
+                      uint16_t((o << (sbits + tbits)) | (unsigned(s) << tbits) | t);
+                } else {
+                  static_cast<int32_t*>(idx)[base + cnt] = perm[b];
+                }
+              }
               ++cnt;
             }
           }
@@ -158,8 +187,8 @@ __global__ void k_rows(const double* __restrict__ spos, const int32_t* __restric
       }
   }
   if (!kFill) {
-    rowcnt[a] = cnt;
-    atomicMax(&flags[1], cnt);
+    if (a0 < n) rowcnt[a] = cnt;
+    wave_atomic_max(&flags[1], cnt);
   }
 }
 
@@ -298,8 +327,8 @@ hipError_t launch_bin(const double* pos, const int32_t* types, int64_t n, const 
 }
 
 hipError_t launch_scatter(const int32_t* key, int64_t n, const int32_t* cell_start, int32_t* fill, int32_t* perm,
-                          hipStream_t s) {
-  k_scatter<<<blocks_for(n, 256), 256, 0, s>>>(key, n, cell_start, fill, perm);
+                          int32_t* flags, hipStream_t s) {
+  k_scatter<<<blocks_for(n, 256), 256, 0, s>>>(key, n, cell_start, fill, perm, flags);
   return hipGetLastError();
 }
 
@@ -315,12 +344,15 @@ hipError_t launch_gather_sorted(const double* pos, const int32_t* perm, int64_t 
 }
 
 hipError_t launch_rows(const double* spos, const int32_t* perm, int64_t n, const NbrGrid& g,
-                       const int32_t* cell_start, int32_t* rowcnt, const int64_t* offsets, int32_t* idx,
-                       int32_t* flags, bool fill, hipStream_t s) {
-  if (fill)
-    k_rows<true><<<blocks_for(n, 128), 128, 0, s>>>(spos, perm, n, g, cell_start, rowcnt, offsets, idx, flags);
+                       const int32_t* cell_start, int32_t* rowcnt, const int64_t* offsets, void* idx,
+                       int32_t* flags, bool fill, int tbits, int sbits, hipStream_t s) {
+  const unsigned nb = blocks_for(n, 128);
+  if (!fill)
+    k_rows<false, false><<<nb, 128, 0, s>>>(spos, perm, n, g, cell_start, rowcnt, offsets, idx, flags, 0, 0);
+  else if (tbits > 0)
+    k_rows<true, true><<<nb, 128, 0, s>>>(spos, perm, n, g, cell_start, rowcnt, offsets, idx, flags, tbits, sbits);
   else
-    k_rows<false><<<blocks_for(n, 128), 128, 0, s>>>(spos, perm, n, g, cell_start, rowcnt, offsets, idx, flags);
+    k_rows<true, false><<<nb, 128, 0, s>>>(spos, perm, n, g, cell_start, rowcnt, offsets, idx, flags, 0, 0);
   return hipGetLastError();
 }
 

@@ -43,9 +43,11 @@ __global__ __launch_bounds__(kBlock) void k_setup(UnfusedArgs A) {
   const int lane = threadIdx.x & 63;
   const long long o = A.perm[a];
   const double xi = A.pos[3 * o], yi = A.pos[3 * o + 1], zi = A.pos[3 * o + 2];
+  int cand[9];
+  if (A.list.idx16) centre_cells(A.list, A.list.key[o], cand);
   const long long e1 = A.offsets[a + 1];
   for (long long e = A.offsets[a] + lane; e < e1; e += 64) {
-    const long long j = A.idx[e];
+    const long long j = list_entry(A.list, cand, e);
     const double dx = fold(A.pos[3 * j] - xi, A.box[0], A.inv_box[0]);
     const double dy = fold(A.pos[3 * j + 1] - yi, A.box[1], A.inv_box[1]);
     const double dz = fold(A.pos[3 * j + 2] - zi, A.box[2], A.inv_box[2]);
@@ -222,6 +224,8 @@ __global__ __launch_bounds__(kBlock) void k_force(UnfusedArgs A) {
   const R* __restrict__ V = static_cast<const R*>(A.V);
   const R* __restrict__ ja = static_cast<const R*>(A.jang);
   double fi[3] = {0, 0, 0}, wi[9] = {0, 0, 0, 0, 0, 0, 0, 0, 0};
+  int cand[9];
+  if (A.list.idx16) centre_cells(A.list, A.list.key[A.perm[a]], cand);
   const long long e1 = A.offsets[a + 1];
   for (long long e = A.offsets[a] + lane; e < e1; e += 64) {
     const double4 v = reinterpret_cast<const double4*>(A.geo)[e];
@@ -239,7 +243,7 @@ __global__ __launch_bounds__(kBlock) void k_force(UnfusedArgs A) {
     }
     const R ir = R(1) / R(v.w);
     const double f[3] = {double(s * R(v.x) * ir + tx), double(s * R(v.y) * ir + ty), double(s * R(v.z) * ir + tz)};
-    const long long j = A.idx[e];
+    const long long j = list_entry(A.list, cand, e);
 #pragma unroll
     for (int d = 0; d < 3; ++d) {
       atomicAdd(&A.forces[3 * j + d], -f[d]);

@@ -331,3 +331,52 @@ def test_md_trajectory_per_step_parity():
         log(f"[md] step {step}: max|dF|={err:.3e} |F|max={np.abs(r['F']).max():.1f}")
         assert err <= TOL
     pot.close()
+
+
+@pytest.mark.parametrize("name,n,over", [("fcc-hea6-128", 5, {}), ("bcc-unary-32", 6, {}),
+                                         ("fcc-binary-4", None, {"lmax": 5, "k": 64})])
+def test_coded_and_index_lists_agree(name, n, over):
+    """The 2-byte coded list (cell choice, species, place in the bucket) and
+    the 4-byte index list give the same rows and results; the default
+    builds the coded one."""
+    torch = pytest.importorskip("torch")
+    from paper_2608_16329_amd import Potential, binding
+    w = synth.make_workload(name, seed=12, n=n, hp_overrides=over)
+    out = {}
+    for fmt in (binding.MLIP_LIST_AUTO, binding.MLIP_LIST_INDEX):
+        pot = Potential(w.hp, w.weights)
+        pot.set_list_format(fmt)
+        pos = to_dev(w.pos)
+        pot.build_neighbors(pos, to_dev(w.types), w.box)
+        N = len(w.pos)
+        F = torch.empty((N, 3), dtype=torch.float64, device="cuda:0")
+        E = torch.empty(N, dtype=torch.float64, device="cuda:0")
+        pot.compute(pos, F, E)
+        torch.cuda.synchronize()
+        out[fmt] = (pot.stats(), pot.neighbors(), F.cpu().numpy(), E.cpu().numpy(),
+                    pot.neighbor_rows(np.arange(0, N, 7)))
+        pot.close()
+    (sa, (oa, ia), Fa, Ea, ra), (sb, (ob, ib), Fb, Eb, rb) = out[0], out[1]
+    log(f"[list] {name}: entry bytes {sa['list_entry_bytes']} / {sb['list_entry_bytes']}, "
+        f"device bytes {sa['device_bytes']} / {sb['device_bytes']}")
+    assert sa["list_entry_bytes"] == 2 and sb["list_entry_bytes"] == 4
+    assert sa["device_bytes"] < sb["device_bytes"]
+    assert_same_neighbor_sets(oa, ia, ob, ib)
+    for x, y in zip(ra, rb):
+        assert np.array_equal(np.sort(x), np.sort(y))
+    assert max_abs(Fa, Fb) <= 1e-12 * max(1.0, np.abs(Fb).max()) and max_abs(Ea, Eb) <= 1e-12 * max(1.0, np.abs(Eb).max())
+
+
+def test_bucket_too_large_for_the_code_falls_back_to_indices():
+    """Sixteen species leave 7 bits for the place in a bucket (128 atoms): a
+    dense cluster of 300 atoms of one species in one cell makes the builder
+    store 4-byte indices; rows and results still match the oracle."""
+    rng = np.random.default_rng(9)
+    hp = synth.HParams(n_species=16, enc_cond=0, reg_cond=0)
+    box = np.array([30.0, 30.0, 30.0])
+    pos = 3.0 + rng.uniform(0.0, 3.5, (300, 3))        # one 7.5 A cell of the 30 A box
+    pos = np.concatenate([pos, 15.0 + rng.uniform(0.0, 12.0, (60, 3))])
+    types = np.concatenate([np.zeros(300, np.int32), rng.integers(1, 16, 60).astype(np.int32)])
+    wts = synth.random_weights(hp, 5, 0.2)
+    g, _ = _compare(hp, wts, pos, types, box, "dense bucket")
+    assert g["stats"]["list_entry_bytes"] == 4
