@@ -9,6 +9,8 @@ compared as sets, bit for bit, against the exact definition applied to the
 caller's coordinates.  MD runs use the head-output scale of the benchmark
 (forces of a trained potential's size); step-0 checks use the unscaled
 weights, whose larger forces make the same absolute tolerance stricter."""
+import os
+
 import numpy as np
 import pytest
 
@@ -40,8 +42,9 @@ def _check_cube(label, pot, m, pos_h, types_h, box, F, E, V, centre, half, n_row
     log(f"[large] {label}: oracle on the cube of half-edge {half} A around {np.round(centre, 2).tolist()}")
     atoms, oE, oF, oV = oracle_cube(m, pos_h, types_h, box, centre, half, index=index)
     sel = torch.from_numpy(atoms).to(F.device)
-    gE, gF, gV = E[sel].cpu().numpy(), F[sel].cpu().numpy(), V[sel].cpu().numpy()
-    eE, eF, eV = max_abs(gE, oE), max_abs(gF, oF), max_abs(gV, oV)
+    gE, gF = E[sel].cpu().numpy(), F[sel].cpu().numpy()
+    eE, eF = max_abs(gE, oE), max_abs(gF, oF)
+    eV = max_abs(V[sel].cpu().numpy(), oV) if V is not None else 0.0   # per-atom virial not requested
     log(f"[large] {label}: {len(atoms)} atoms, max|dE|={eE:.3e} max|dF|={eF:.3e} max|dW|={eV:.3e} "
         f"(|F|max={np.abs(oF).max():.2f})")
     assert len(atoms) >= 2000
@@ -188,18 +191,16 @@ def test_bcc_unary_65k_full_md_steps_0_50_100():
     pot.close()
 
 
-def test_bcc_sweep_edge_l384_list_beyond_2_31_entries():
-    """The capacity-sweep alloy (six-component BCC, a = 3.2 A) at L = 384:
-    113,246,208 atoms whose neighbour list holds about 7.1e9 entries, beyond
-    the 2^31 of a 32-bit offset.  A cube of more than 2,000 atoms and 2,000
-    rows against the oracle, with only the atoms near the cube copied to the
-    host."""
+def _sweep_edge(L, precision):
+    """The capacity-sweep alloy (six-component BCC, a = 3.2 A) at edge L, its
+    positions generated straight into device memory: a cube of more than
+    2,000 atoms and 2,000 rows against the oracle (R24's bar in float32),
+    with only the atoms near the cube copied to the host."""
     import torch
     from paper_2608_16329_amd import Potential
     p = synth.PRESETS["bcc-hea6-sweep"]
-    L = 384
     N = 2 * L ** 3
-    hp = synth.HParams(n_species=p["C"], cutoff=p["cutoff"], skin=0.5)
+    hp = synth.HParams(n_species=p["C"], cutoff=p["cutoff"], skin=0.5, precision=precision)
     weights = synth.random_weights(hp, 1)
     masses = np.array([synth.MASS[x] for x in p["masses"]])
     box = np.array([L * p["a"]] * 3)
@@ -216,13 +217,18 @@ def test_bcc_sweep_edge_l384_list_beyond_2_31_entries():
     log(f"[large] L={L} N={N}: build")
     pot.build_neighbors(pos, types, box)
     st = pot.stats()
-    log(f"[large] L={L}: {st['n_listed_pairs']} listed entries")
+    log(f"[large] L={L}: {st['n_listed_pairs']} listed entries of {st['list_entry_bytes']} bytes, "
+        f"library {pot.memory_bytes() / N:.0f} B per atom")
     assert st["n_listed_pairs"] > 2 ** 31
-    F, E, V = _outputs(N)
-    log(f"[large] L={L}: compute")
+    F = torch.zeros((N, 3), dtype=torch.float64, device=dev)
+    E = torch.zeros(N, dtype=torch.float64, device=dev)
+    # above 3e8 atoms the sweep keeps no per-atom virial (totals only)
+    V = torch.zeros((N, 9), dtype=torch.float64, device=dev) if N <= 300_000_000 else None
+    log(f"[large] L={L}: compute (float{precision})")
     pot.compute(pos, F, E, V)
     torch.cuda.synchronize()
-    centre = np.array([142.0, 200.0, 311.0]) * p["a"]   # a lattice site deep inside, not at an end of the order
+    centre = np.array([0.37, 0.52, 0.81]) * L     # in cells: a lattice site deep inside, not at an end of the order
+    centre = np.floor(centre) * p["a"]
     half = 16.5
     m = Model(hp, weights)
     reach = half + 2.0 * (m.rc + m.skin) + 1.0
@@ -233,11 +239,35 @@ def test_bcc_sweep_edge_l384_list_beyond_2_31_entries():
     near = torch.nonzero((d.abs() < reach).all(dim=1)).squeeze(1)
     del d
     index = near.cpu().numpy()
-    _check_cube(f"bcc sweep L={L}", pot, m, pos[near].cpu().numpy(), types[near].cpu().numpy(), box, F, E, V,
-                centre, half, 2000, index=index)
+    if precision == 64:
+        _check_cube(f"bcc sweep L={L}", pot, m, pos[near].cpu().numpy(), types[near].cpu().numpy(), box, F, E, V,
+                    centre, half, 2000, index=index)
+    else:
+        atoms, oE, oF, oV = oracle_cube(m, pos[near].cpu().numpy(), types[near].cpu().numpy(), box, centre, half,
+                                        index=index)
+        sel = torch.from_numpy(atoms).to(dev)
+        errs = [max_abs(g[sel].cpu().numpy(), o) / max(1.0, float(np.abs(o).max()))
+                for g, o in ((E, oE), (F, oF), (V, oV)) if g is not None] + [0.0]
+        log(f"[large] bcc sweep L={L} float32: {len(atoms)} atoms, rel dE={errs[0]:.2e} dF={errs[1]:.2e} "
+            f"dW={errs[2]:.2e}")
+        assert len(atoms) >= 2000 and max(errs) <= 1e-4
     pot.close()
     del pos, types, F, E, V
     torch.cuda.empty_cache()
+
+
+def test_bcc_sweep_edge_l384_list_beyond_2_31_entries():
+    """L = 384: 113,246,208 atoms whose neighbour list holds about 7.1e9
+    entries, beyond the 2^31 of a 32-bit offset."""
+    _sweep_edge(384, 64)
+
+
+@pytest.mark.skipif(not os.environ.get("MLIP_SWEEP_EDGE"), reason="opt-in: MLIP_SWEEP_EDGE=<L>:<precision>")
+def test_bcc_sweep_edge_opt_in():
+    """A larger sweep edge on request (minutes of host-side generation, one
+    evaluation of up to a billion atoms): MLIP_SWEEP_EDGE=L:precision."""
+    L, precision = (int(x) for x in os.environ["MLIP_SWEEP_EDGE"].split(":"))
+    _sweep_edge(L, precision)
 
 
 def test_bcc_sweep_shape_l128_cube():
