@@ -155,15 +155,16 @@ def summarize_traffic(fetch_dir: str, write_dir: str, bench_log: str, copy_bytes
     print(json.dumps(t))
 
 
-def neighbour_build_record(events, first_ms: float, n_atoms: int, n_listed: int) -> dict:
+def neighbour_build_record(events, first_ms: float, n_atoms: int, n_listed: int,
+                           entry_bytes: int) -> dict:
     """Time and bandwidth of the neighbour-list build: HIP events around the
     rebuilds of the timed steps (the first build's wall time when none fell
     there).  Algorithmic bytes: positions and species read (28 B per atom),
     cell keys, permutation, sorted positions, row counts and int64 offsets
-    written (44 B per atom), 4 B per listed entry written; candidate positions
-    are re-read from cache and not counted."""
+    written (44 B per atom), one entry (2 B coded, 4 B as an index) per listed
+    pair written; candidate positions are re-read from cache and not counted."""
     ms = float(np.mean([a.elapsed_time(b) for a, b in events])) if events else first_ms
-    nbytes = 72.0 * n_atoms + 4.0 * n_listed
+    nbytes = 72.0 * n_atoms + float(entry_bytes) * n_listed
     return {"ms": ms, "timed_rebuilds": len(events), "algorithmic_bytes": nbytes,
             "gbps": nbytes / (ms * 1e-3) / 1e9, "frac_of_hbm": nbytes / (ms * 1e-3) / 1e9 / PEAK_HBM_GBS,
             "bound": "candidate scan (27 cells, about 500 distance tests per atom, twice)"}
@@ -263,6 +264,7 @@ def capacity_sweep(edges, steps: int, seed: int, bpa: float = 450.0, precision: 
                           "device_total_bytes": total, "rebuilds_in_timed_steps": rebuilds,
                           "build_s": t_build, "listed_pairs_per_atom": st["n_listed_pairs"] / N,
                           "active_pairs_per_atom": st["n_active_pairs"] / N,
+                          "list_entry_bytes": st["list_entry_bytes"],
                           "max_atoms_estimate": int(0.97 * total / bpa)}), flush=True)
         pot.close()
         del pos, vel, types, F
@@ -387,6 +389,9 @@ def main() -> int:
     ap.add_argument("--scatter", choices=("atomic", "tile"), default="atomic",
                     help="F_j scatter of the cached kernel: one atomic per pair (default) or summed per distinct "
                          "neighbour of a tile in LDS first")
+    ap.add_argument("--list", choices=("auto", "index"), default="auto",
+                    help="neighbour-list entries: 2-byte codes where the cell buckets allow (default) or 4-byte "
+                         "indices")
     ap.add_argument("--hp", default="",
                     help="comma-separated hyper-parameter overrides, e.g. k=64,lmax=2,enc_cond=1")
     ap.add_argument("--rebuild-every", type=int, default=10)
@@ -454,6 +459,7 @@ def main() -> int:
     pot = Potential(w.hp, w.weights, stream=stream)
     pot.set_fusion({"cached": 0, "recompute": 1, "partial": 2, "unfused": 3}[args.fusion])
     pot.set_scatter({"atomic": 0, "tile": 1}[args.scatter])
+    pot.set_list_format({"auto": 0, "index": 1}[args.list])
     pot.set_masses(w.masses)
     t0 = time.perf_counter()
     pot.build_neighbors(pos, types, w.box)
@@ -522,11 +528,14 @@ def main() -> int:
     used = free0 - free1
     bpa = used / N
 
-    traffic = measured_traffic(w.description, N, args.precision, args.fusion) if args.scatter == "atomic" else None
+    traffic = (measured_traffic(w.description, N, args.precision, args.fusion)
+               if args.scatter == "atomic" and args.list == "auto" else None)
     recompute = None
     if args.fusion == "cached" and args.recompute_evals > 0 and w.hp.k == 32 and w.hp.lmax <= 3 \
             and w.hp.angular == 0:
         recompute = recompute_record(pot, pos, F, E, V, stream, args.recompute_evals, flop, N, w, args.precision)
+        if args.list != "auto":   # the committed traffic summary was taken with the default list entries
+            recompute["traffic"] = recompute["traffic_gbps"] = None
     result = {
         "metric": "atom-steps/s (E+F+virial) at 1 GPU",
         "value": value,
@@ -548,7 +557,8 @@ def main() -> int:
                    "listed_pairs_per_atom": st["n_listed_pairs"] / N, "tile_atoms": st["tile_atoms"],
                    "blocks": st["n_blocks"], "seed": args.seed, "precision": args.precision,
                    "enc_cond": w.hp.enc_cond, "reg_cond": w.hp.reg_cond, "enc_hidden": w.hp.enc_hidden,
-                   "reg_hidden": w.hp.reg_hidden, "fusion": args.fusion, "scatter": args.scatter},
+                   "reg_hidden": w.hp.reg_hidden, "fusion": args.fusion, "scatter": args.scatter,
+                   "list_entry_bytes": st["list_entry_bytes"]},
         "roofline": {"bound": "mfma", "achieved": achieved, "peak": PEAK_TFLOPS[args.precision], "unit": "TFLOP/s",
                      "frac": achieved / PEAK_TFLOPS[args.precision],
                      "traffic": traffic,
@@ -567,7 +577,8 @@ def main() -> int:
         "caller_bytes_per_atom": caller_bytes / N,
         "max_atoms_estimate": int(0.95 * total_mem / bpa),
         "build_ms": t_build * 1e3,
-        "neighbour_build": neighbour_build_record(rebuild_ms, t_build * 1e3, N, st["n_listed_pairs"]),
+        "neighbour_build": neighbour_build_record(rebuild_ms, t_build * 1e3, N, st["n_listed_pairs"],
+                                                  st["list_entry_bytes"]),
     }
     if args.cpu_sample > 0:
         log("[bench] timing the oracle on a bounded sample")

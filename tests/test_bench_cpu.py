@@ -24,9 +24,10 @@ def test_flops_per_pair_and_atom_closed_forms():
 
 
 def test_neighbour_build_record_without_timed_rebuilds():
-    r = bench.neighbour_build_record([], 40.0, 1000, 90_000)
+    r = bench.neighbour_build_record([], 40.0, 1000, 90_000, 4)
     assert r["ms"] == 40.0 and r["timed_rebuilds"] == 0
     assert r["algorithmic_bytes"] == 72 * 1000 + 4 * 90_000
+    assert bench.neighbour_build_record([], 40.0, 1000, 90_000, 2)["algorithmic_bytes"] == 72 * 1000 + 2 * 90_000
     assert abs(r["gbps"] - r["algorithmic_bytes"] / 0.040 / 1e9) < 1e-12
     assert abs(r["frac_of_hbm"] - r["gbps"] / bench.PEAK_HBM_GBS) < 1e-15
 
