@@ -363,6 +363,25 @@ struct FragStream {
   }
 };
 
+// Bias vector of a hidden layer at a wave-uniform address, read through a
+// buffer descriptor in the accumulator row order: element (To, q) of lane
+// (g, c) is row 16 To + drow(q, g); the lane part of that offset is one
+// fixed vector register, the rest a scalar offset.  With bytes = 0 every
+// read returns zero without touching memory.
+template <typename R>
+struct BiasStream {
+  __amdgpu_buffer_rsrc_t rs;
+  int lo;
+  __device__ __forceinline__ BiasStream(const void* base, int bytes, int g)
+      : rs(__builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, bytes, kRawBufferConfig)),
+        lo((sizeof(R) == 8 ? g : 4 * g) * int(sizeof(R))) {}
+  __device__ __forceinline__ R operator()(int To, int q) const {
+    const int so = (16 * To + (sizeof(R) == 8 ? 4 * q : q)) * int(sizeof(R));
+    if constexpr (sizeof(R) == 8) return __builtin_bit_cast(R, __builtin_amdgcn_raw_buffer_load_b64(rs, lo, so, 0));
+    else return __builtin_bit_cast(R, __builtin_amdgcn_raw_buffer_load_b32(rs, lo, so, 0));
+  }
+};
+
 template <int K, typename R>
 struct Stream {
   static constexpr int KT = K / 16;
@@ -418,6 +437,24 @@ __device__ __forceinline__ const R* encoder_hidden(const FusedArgs& A, const Sme
   typedef typename St::vh_t vh_t;
   constexpr int NH = St::NH, VW = St::VW, kRing = St::kRing;
   const int lane = threadIdx.x & 63, g = lane >> 4;
+  constexpr int kLayerBytes = int(kEncWidth * kEncWidth * sizeof(R));
+  constexpr int kBiasBytes = int(kEncWidth * sizeof(R));
+  const int nh = A.enc_hidden;
+  // The first hidden layer's leading weight fragments are requested before
+  // the elementwise first layer, whose activation work covers their
+  // latency; each hidden layer requests the next one's in its last k-steps,
+  // so they arrive during its own activation phase.  Past the last hidden
+  // layer that descriptor has size 0 and reads zeros.
+  const R* __restrict__ layer = tab + 2 * kEncWidth;
+  vh_t wb[kRing][NH];
+  v4<R> acc[8], dacc[8];
+  {
+    const FragStream<vh_t> frag(layer, nh > 1 ? kLayerBytes : 0);
+#pragma unroll
+    for (int p = 0; p < kRing - 1; ++p)
+#pragma unroll
+      for (int u = 0; u < NH; ++u) wb[p][u] = frag[p * NH + u];
+  }
 #pragma unroll
   for (int T = 0; T < 8; ++T)
 #pragma unroll
@@ -428,29 +465,24 @@ __device__ __forceinline__ const R* encoder_hidden(const FusedArgs& A, const Sme
       h[T][i] = z * s;
       if constexpr (kTan) dh[T][i] = s * (R(1) + z * (R(1) - s)) * w0;
     }
-  const R* __restrict__ layer = tab + 2 * kEncWidth;
-  for (int t = 1; t < A.enc_hidden; ++t) {
-    const FragStream<vh_t> frag(layer, int(kEncWidth * kEncWidth * sizeof(R)));
-    const R* __restrict__ bias = layer + kEncWidth * kEncWidth;
-    vh_t wb[kRing][NH];
+  for (int t = 1; t < nh; ++t) {
+    const FragStream<vh_t> frag(layer, kLayerBytes);
+    const R* __restrict__ next = layer + kEncWidth * kEncWidth + kEncWidth;
+    const bool more = t + 1 < nh;
+    const FragStream<vh_t> nfrag(next, more ? kLayerBytes : 0);
+    // the tangent has no bias
+    {
+      const BiasStream<R> bias(layer + kEncWidth * kEncWidth, kBiasBytes, g);
 #pragma unroll
-    for (int p = 0; p < kRing - 1; ++p)
-#pragma unroll
-      for (int u = 0; u < NH; ++u) wb[p][u] = frag[p * NH + u];
-    // the forward accumulators start from the bias; the tangent has none
-    v4<R> acc[8], dacc[8];
-#pragma unroll
-    for (int To = 0; To < 8; ++To) {
-      acc[To] = v4<R>{bias[16 * To + drow<R>(0, g)], bias[16 * To + drow<R>(1, g)], bias[16 * To + drow<R>(2, g)],
-                      bias[16 * To + drow<R>(3, g)]};
-      dacc[To] = v4<R>{0, 0, 0, 0};
+      for (int To = 0; To < 8; ++To) acc[To] = v4<R>{bias(To, 0), bias(To, 1), bias(To, 2), bias(To, 3)};
     }
 #pragma unroll
-    for (int ks = 0; ks < 32; ++ks) {
-      if (ks + kRing - 1 < 32) {
+    for (int To = 0; To < 8; ++To) dacc[To] = v4<R>{0, 0, 0, 0};
 #pragma unroll
-        for (int u = 0; u < NH; ++u) wb[(ks + kRing - 1) % kRing][u] = frag[(ks + kRing - 1) * NH + u];
-      }
+    for (int ks = 0; ks < 32; ++ks) {
+      const int kn = ks + kRing - 1;
+#pragma unroll
+      for (int u = 0; u < NH; ++u) wb[kn % kRing][u] = kn < 32 ? frag[kn * NH + u] : nfrag[(kn - 32) * NH + u];
       __builtin_amdgcn_sched_barrier(0);
       const int T = ks >> 2, i = ks & 3;
 #pragma unroll
@@ -461,9 +493,21 @@ __device__ __forceinline__ const R* encoder_hidden(const FusedArgs& A, const Sme
       }
       __builtin_amdgcn_sched_barrier(0);
     }
-    layer += kEncWidth * kEncWidth + kEncWidth;
+    // the next layer's k-step p sits in slot (32 + p) mod kRing; it starts
+    // from slot p (a no-op when kRing divides 32)
+    if constexpr (32 % kRing != 0) {
+      vh_t nx[kRing - 1][NH];
 #pragma unroll
-    for (int To = 0; To < 8; ++To)
+      for (int p = 0; p < kRing - 1; ++p)
+#pragma unroll
+        for (int u = 0; u < NH; ++u) nx[p][u] = wb[(32 + p) % kRing][u];
+#pragma unroll
+      for (int p = 0; p < kRing - 1; ++p)
+#pragma unroll
+        for (int u = 0; u < NH; ++u) wb[p][u] = nx[p][u];
+    }
+#pragma unroll
+    for (int To = 0; To < 8; ++To) {
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
         const R z = acc[To][q];
@@ -471,6 +515,8 @@ __device__ __forceinline__ const R* encoder_hidden(const FusedArgs& A, const Sme
         h[To][q] += z * s;
         if constexpr (kTan) dh[To][q] += s * (R(1) + z * (R(1) - s)) * dacc[To][q];
       }
+    }
+    layer = next;
   }
   return layer;
 }

@@ -234,10 +234,14 @@ def _sweep_edge(L, precision):
     reach = half + 2.0 * (m.rc + m.skin) + 1.0
     c = torch.from_numpy(centre).to(dev)
     bt = torch.from_numpy(box).to(dev)
-    d = pos - c
-    d -= bt * torch.round(d / bt)
-    near = torch.nonzero((d.abs() < reach).all(dim=1)).squeeze(1)
-    del d
+    near = []
+    step = 1 << 25    # slabs of rows: no full-size temporaries beside a billion atoms
+    for s0 in range(0, N, step):
+        d = pos[s0:s0 + step] - c
+        d -= bt * torch.round(d / bt)
+        near.append(torch.nonzero((d.abs() < reach).all(dim=1)).squeeze(1) + s0)
+        del d
+    near = torch.cat(near)
     index = near.cpu().numpy()
     if precision == 64:
         _check_cube(f"bcc sweep L={L}", pot, m, pos[near].cpu().numpy(), types[near].cpu().numpy(), box, F, E, V,
