@@ -246,9 +246,15 @@ __device__ __forceinline__ void monomials_n(R x, R y, R z, R m[NM], R gx[NM], R 
 // up to 32 atoms has a few hundred distinct neighbours.
 constexpr int kFjSlots = 1024;
 
+// Rows of the moment kept in LDS: the angular rows of the configuration (16
+// irreducible rows to l_max 3, the Cartesian basis's 20, 36 to l_max 5) of
+// the DR rows that its 16-row MFMA tiles span; the rows past them are zero
+// in every product and are neither stored nor read.
+constexpr int moment_rows(int DR, int NM) { return NM == 56 ? 36 : (DR == 32 ? 20 : DR); }
+
 template <int K, int TM, typename R, int NW, int DR, int NM>
 struct Smem {
-  R P[TM][DR][K + 1];  // moment, then its adjoint W (padded rows)
+  R P[TM][moment_rows(DR, NM)][K + 1];  // moment, then its adjoint W (padded columns)
   // Pass 1 reads the first-layer weights; the head runs after pass 1 and
   // before the next tile is staged, so its activations reuse those bytes.
   union {
@@ -687,10 +693,14 @@ __device__ void pass1_chunk(const FusedArgs& A, Smem<K, TM, R, NW, DR, NM>& S, i
 #pragma unroll
         for (int Tc = 0; Tc < KT; ++Tc) pacc[Tc] = mfma(av_a, mo[Tc][q], pacc[Tc]);
       }
+      constexpr int DRS = moment_rows(DR, NM);
 #pragma unroll
       for (int Tc = 0; Tc < KT; ++Tc)
 #pragma unroll
-        for (int q = 0; q < 4; ++q) atomicAdd(&S.P[a][16 * ta + drow<R>(q, g)][16 * Tc + c], pacc[Tc][q]);
+        for (int q = 0; q < 4; ++q) {
+          const int row = 16 * ta + drow<R>(q, g);
+          if (16 * ta + 16 <= DRS || row < DRS) atomicAdd(&S.P[a][row][16 * Tc + c], pacc[Tc][q]);
+        }
     }
   }
 
@@ -826,7 +836,8 @@ __device__ void pass2_chunk(const FusedArgs& A, Smem<K, TM, R, NW, DR, NM>& S, i
       for (int Tc = 0; Tc < KT; ++Tc)
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          const R w = S.P[a][16 * ta + c][16 * Tc + drow<R>(i, g)];
+          constexpr int DRS = moment_rows(DR, NM);
+          const R w = 16 * ta + 16 <= DRS || 16 * ta + c < DRS ? S.P[a][16 * ta + c][16 * Tc + drow<R>(i, g)] : R(0);
           t1 = mfma(w, in.mB[Tc][i], t1);
           t2 = mfma(w, in.dmB[Tc][i], t2);
         }
@@ -1311,11 +1322,12 @@ __global__ __launch_bounds__(64 * NW, 1) void k_fused(FusedArgs A) {
     }
     for (int u = tid; u < kMaxSpecies * TM; u += (64 * NW)) S.cnt[u / TM][u % TM] = 0;
     if constexpr (MODE != kRadial)
-      for (int u = tid; u < TM * DR * (K + 1); u += (64 * NW)) (&S.P[0][0][0])[u] = R(0);
+      for (int u = tid; u < TM * moment_rows(DR, NM) * (K + 1); u += (64 * NW)) (&S.P[0][0][0])[u] = R(0);
     __syncthreads();
     const int nent = S.ent_base[na];
     const long long ebase = S.row_beg[0];
     constexpr int kPer = tile_entry_cap(TM) / (64 * NW);
+    static_assert(kPer * 64 * NW == tile_entry_cap(TM), "every listed entry of a tile needs a thread");
     int ej[kPer], ea[kPer], es[kPer];
     int my_active = 0;
     {
@@ -1625,17 +1637,18 @@ void angular_table_shape(int acfg, int* rows, int* cols) {
 
 // Instantiations: k in {16, 32, 64}; float64 with one wavefront per SIMD,
 // float32 with two.  Atoms per tile: float64 16, float32 32 (two column
-// groups in the head), fewer where the moment tiles would not fit LDS: at
-// k = 64 8 (float64) and 16 (float32); the Cartesian basis (k = 32) 8 and
-// 16; l_max 4..5, whose 48-row moment and 6k-wide head input grow with k,
-// 12 / 6 / 2 atoms at k = 16 / 32 / 64 in float64 and 24 / 16 / 8 in
-// float32.  The other fusion configurations are built for k = 32 with the
-// irreducible basis and l_max <= 3.
+// groups in the head), fewer where the moment would not fit LDS: at k = 64
+// 8 (float64) and 16 (float32); l_max 4..5, whose 36-row moment and 6k-wide
+// head input grow with k, 16 / 9 / 3 atoms at k = 16 / 32 / 64 in float64
+// and 32 / 16 / 11 in float32 (a tile's listed entries are spread evenly
+// over the work-group's threads, which rules out 17-19 at k = 32).  The
+// other fusion configurations are built for k = 32 with the irreducible
+// basis and l_max <= 3.
 int fused_tile_max(int k, int precision, int acfg) {
-  if (acfg == 1) return precision == 64 ? 8 : 16;
+  if (acfg == 1) return precision == 64 ? 16 : 32;
   if (acfg == 2) {
-    if (precision == 64) return k == 16 ? 12 : (k == 32 ? 6 : 2);
-    return k == 16 ? 24 : (k == 32 ? 16 : 8);
+    if (precision == 64) return k == 16 ? 16 : (k == 32 ? 9 : 3);
+    return k == 16 ? 32 : (k == 32 ? 16 : 11);
   }
   if (precision == 64) return k == 64 ? 8 : 16;
   return k == 64 ? 16 : 32;
@@ -1645,12 +1658,12 @@ hipError_t launch_fused(int k, int precision, int acfg, int mode, const FusedArg
   if (mode != kCached && (k != 32 || acfg != 0)) return hipErrorInvalidValue;
   if (acfg == 1 && k != 32) return hipErrorInvalidValue;
   if (precision == 64) {
-    if (acfg == 1) return launch_k<32, 8, double, 4, 32, 20, kCached>(a, n_blocks, s);
+    if (acfg == 1) return launch_k<32, 16, double, 4, 32, 20, kCached>(a, n_blocks, s);
     if (acfg == 2) {
       switch (k) {
-        case 16: return launch_k<16, 12, double, 4, 48, 56, kCached>(a, n_blocks, s);
-        case 32: return launch_k<32, 6, double, 4, 48, 56, kCached>(a, n_blocks, s);
-        case 64: return launch_k<64, 2, double, 4, 48, 56, kCached>(a, n_blocks, s);
+        case 16: return launch_k<16, 16, double, 4, 48, 56, kCached>(a, n_blocks, s);
+        case 32: return launch_k<32, 9, double, 4, 48, 56, kCached>(a, n_blocks, s);
+        case 64: return launch_k<64, 3, double, 4, 48, 56, kCached>(a, n_blocks, s);
         default: return hipErrorInvalidValue;
       }
     }
@@ -1661,12 +1674,12 @@ hipError_t launch_fused(int k, int precision, int acfg, int mode, const FusedArg
       default: break;
     }
   } else if (precision == 32) {
-    if (acfg == 1) return launch_k<32, 16, float, 8, 32, 20, kCached>(a, n_blocks, s);
+    if (acfg == 1) return launch_k<32, 32, float, 8, 32, 20, kCached>(a, n_blocks, s);
     if (acfg == 2) {
       switch (k) {
-        case 16: return launch_k<16, 24, float, 8, 48, 56, kCached>(a, n_blocks, s);
+        case 16: return launch_k<16, 32, float, 8, 48, 56, kCached>(a, n_blocks, s);
         case 32: return launch_k<32, 16, float, 8, 48, 56, kCached>(a, n_blocks, s);
-        case 64: return launch_k<64, 8, float, 8, 48, 56, kCached>(a, n_blocks, s);
+        case 64: return launch_k<64, 11, float, 8, 48, 56, kCached>(a, n_blocks, s);
         default: return hipErrorInvalidValue;
       }
     }
