@@ -450,11 +450,14 @@ __device__ __forceinline__ const R* encoder_hidden(const FusedArgs& A, const Sme
   // the elementwise first layer, whose activation work covers their
   // latency; each hidden layer requests the next one's in its last k-steps,
   // so they arrive during its own activation phase.  Past the last hidden
-  // layer that descriptor has size 0 and reads zeros.
+  // layer that descriptor has size 0 and reads zeros.  At k = 64 the wider
+  // output tiles leave no registers for fragments held across an activation
+  // phase (it measured slower): there each layer fills its ring at its start.
+  constexpr bool kCross = K <= 32;
   const R* __restrict__ layer = tab + 2 * kEncWidth;
   vh_t wb[kRing][NH];
   v4<R> acc[8], dacc[8];
-  {
+  if constexpr (kCross) {
     const FragStream<vh_t> frag(layer, nh > 1 ? kLayerBytes : 0);
 #pragma unroll
     for (int p = 0; p < kRing - 1; ++p)
@@ -476,6 +479,12 @@ __device__ __forceinline__ const R* encoder_hidden(const FusedArgs& A, const Sme
     const R* __restrict__ next = layer + kEncWidth * kEncWidth + kEncWidth;
     const bool more = t + 1 < nh;
     const FragStream<vh_t> nfrag(next, more ? kLayerBytes : 0);
+    if constexpr (!kCross) {
+#pragma unroll
+      for (int p = 0; p < kRing - 1; ++p)
+#pragma unroll
+        for (int u = 0; u < NH; ++u) wb[p][u] = frag[p * NH + u];
+    }
     // the tangent has no bias
     {
       const BiasStream<R> bias(layer + kEncWidth * kEncWidth, kBiasBytes, g);
@@ -487,8 +496,10 @@ __device__ __forceinline__ const R* encoder_hidden(const FusedArgs& A, const Sme
 #pragma unroll
     for (int ks = 0; ks < 32; ++ks) {
       const int kn = ks + kRing - 1;
+      if (kCross || kn < 32) {
 #pragma unroll
-      for (int u = 0; u < NH; ++u) wb[kn % kRing][u] = kn < 32 ? frag[kn * NH + u] : nfrag[(kn - 32) * NH + u];
+        for (int u = 0; u < NH; ++u) wb[kn % kRing][u] = kn < 32 ? frag[kn * NH + u] : nfrag[(kn - 32) * NH + u];
+      }
       __builtin_amdgcn_sched_barrier(0);
       const int T = ks >> 2, i = ks & 3;
 #pragma unroll
@@ -501,7 +512,7 @@ __device__ __forceinline__ const R* encoder_hidden(const FusedArgs& A, const Sme
     }
     // the next layer's k-step p sits in slot (32 + p) mod kRing; it starts
     // from slot p (a no-op when kRing divides 32)
-    if constexpr (32 % kRing != 0) {
+    if constexpr (kCross && 32 % kRing != 0) {
       vh_t nx[kRing - 1][NH];
 #pragma unroll
       for (int p = 0; p < kRing - 1; ++p)
