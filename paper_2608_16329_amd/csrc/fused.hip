@@ -131,6 +131,13 @@ __device__ __forceinline__ float sigmoid(float z) {
   return __builtin_amdgcn_rcpf(1.0f + e);
 }
 
+// Slope of the SiLU z s(z), s (1 + z (1 - s)), as two fused multiply-adds:
+// t = z - s z = z (1 - s), then s + s t.
+template <typename R>
+__device__ __forceinline__ R silu_slope(R z, R s) {
+  return fma(s, fma(-s, z, z), s);
+}
+
 // Pair geometry after the minimum-image difference (which stays in float64):
 // IEEE float64 square root and division, or the float32 hardware
 // instructions (about one ulp).
@@ -472,7 +479,7 @@ __device__ __forceinline__ const R* encoder_hidden(const FusedArgs& A, const Sme
       const R w0 = S.u.l0[sj][0][in], z = w0 * r + S.u.l0[sj][1][in];
       const R s = sigmoid(z);
       h[T][i] = z * s;
-      if constexpr (kTan) dh[T][i] = s * (R(1) + z * (R(1) - s)) * w0;
+      if constexpr (kTan) dh[T][i] = silu_slope(z, s) * w0;
     }
   for (int t = 1; t < nh; ++t) {
     const FragStream<vh_t> frag(layer, kLayerBytes);
@@ -530,7 +537,7 @@ __device__ __forceinline__ const R* encoder_hidden(const FusedArgs& A, const Sme
         const R z = acc[To][q];
         const R s = sigmoid(z);
         h[To][q] += z * s;
-        if constexpr (kTan) dh[To][q] += s * (R(1) + z * (R(1) - s)) * dacc[To][q];
+        if constexpr (kTan) dh[To][q] = fma(silu_slope(z, s), dacc[To][q], dh[To][q]);
       }
     }
     layer = next;
@@ -1183,7 +1190,7 @@ __device__ void head_stage(const FusedArgs& A, Smem<K, TM, R, NW, DR, NM>& S) {
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
           const R z = zeta[t][cg][q], sg = sigmoid(z);
-          S.u.hd.gT[ROW(q)][16 * cg + c] = sg * (R(1) + z * (R(1) - sg)) * d[cg][q];
+          S.u.hd.gT[ROW(q)][16 * cg + c] = silu_slope(z, sg) * d[cg][q];
         }
     }
     __syncthreads();
@@ -1208,7 +1215,7 @@ __device__ void head_stage(const FusedArgs& A, Smem<K, TM, R, NW, DR, NM>& S) {
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
         const R z = z0[cg][q], sg = sigmoid(z);
-        S.u.hd.gT[ROW(q)][16 * cg + c] = sg * (R(1) + z * (R(1) - sg)) * d[cg][q];
+        S.u.hd.gT[ROW(q)][16 * cg + c] = silu_slope(z, sg) * d[cg][q];
       }
   }
   __syncthreads();
