@@ -36,6 +36,21 @@ def traffic_summary_path(precision: int, fusion: str = "cached") -> str:
     return os.path.join(ROOT, "profiles", f"k_fused{tag}_fcc-hea6-128_traffic.md")
 
 
+def largest_system_run():
+    """The largest system the committed capacity-sweep summary records as run
+    on one GPU (atoms, bytes per atom), or None without that summary."""
+    import re
+    try:
+        text = open(os.path.join(ROOT, "profiles", "capacity_sweep_bcc-hea6.md")).read()
+    except OSError:
+        return None
+    m = re.search(r"Largest system run: ([\d,]+) atoms .*?, (\d+) bytes per atom", text)
+    if not m:
+        return None
+    return {"atoms": int(m.group(1).replace(",", "")), "bytes_per_atom": int(m.group(2)),
+            "source": "profiles/capacity_sweep_bcc-hea6.md (6-component BCC, totals only)"}
+
+
 def fused_source_hash() -> str:
     import hashlib
     with open(FUSED_SOURCE, "rb") as f:
@@ -575,7 +590,8 @@ def main() -> int:
         "hbm_bytes_per_atom": bpa,
         "library_bytes_per_atom": lib_bytes / N,
         "caller_bytes_per_atom": caller_bytes / N,
-        "max_atoms_estimate": int(0.95 * total_mem / bpa),
+        "max_atoms_estimate": int(0.95 * total_mem / bpa),   # at this workload's bytes per atom
+        "max_atoms_run": largest_system_run(),
         "build_ms": t_build * 1e3,
         "neighbour_build": neighbour_build_record(rebuild_ms, t_build * 1e3, N, st["n_listed_pairs"],
                                                   st["list_entry_bytes"]),

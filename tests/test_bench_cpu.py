@@ -41,3 +41,8 @@ def test_more_than_one_gpu_is_refused_with_a_message():
                        capture_output=True, text=True, timeout=120)
     assert r.returncode == 2
     assert "one GPU" in r.stderr and not r.stdout.strip()
+
+
+def test_largest_system_run_is_read_from_the_sweep_summary():
+    r = bench.largest_system_run()
+    assert r is not None and r["atoms"] > 10 ** 9 and 100 < r["bytes_per_atom"] < 1000
